@@ -1,0 +1,249 @@
+"""Benchmark of the Approx-BP / MS-BP hot path on one MI355X.
+
+A step is one pass of the whole hot path over one batch of the LLaMA-7B-shaped
+workload (bf16 storage, fp32 arithmetic), in training order:
+
+    MS-RMSNorm forward   on x    [4*2048, 4096]   -> z, rstd
+    ReSiLU2 forward      on gate [4*2048, 11008]  -> SiLU(gate), 2-bit codes
+    ReSiLU2 backward     dy, codes                -> d gate
+    MS-RMSNorm backward  dz, z, rstd              -> dx
+
+Inputs are seeded synthetic tensors already resident in HBM. The reported value
+is the algorithmic HBM traffic of the step (bytes each kernel must read and
+write) divided by the measured step time. Per-kernel durations come from HIP
+events recorded on the stream the kernels run on, inside the timed region.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, AMD published peak
+WORKLOAD = "llama7b_swiglu_bf16"
+METRIC = "fwd+bwd HBM GB/s (% of peak) for ReGELU2/ReSiLU2/MS-LN; saved bytes/elt"
+KERNEL_SOURCES = ("paper_2406_16282_amd/csrc/act_kernels.hip",
+                  "paper_2406_16282_amd/csrc/norm_kernels.hip",
+                  "paper_2406_16282_amd/csrc/lmbp_device.hpp",
+                  "paper_2406_16282_amd/csrc/gelu_poly.h")
+
+
+def algorithmic_bytes(w):
+    """Bytes each kernel must move once (reads + writes), per launch."""
+    eb = 2 if w.norm.dtype == "bf16" else 4
+    rows, p = w.norm.rows, w.norm.cols
+    n_norm = rows * p
+    n_act = w.act.rows * w.act.cols
+    ab = 2 if w.act.dtype == "bf16" else 4
+    codes = 4 * ((n_act + 15) // 16)
+    return {
+        f"{w.norm.op}_fwd": 2 * n_norm * eb + 4 * rows,            # x in, z out, rstd out
+        f"{w.act.op}_fwd": 2 * n_act * ab + codes,                 # x in, y out, codes out
+        f"{w.act.op}_bwd": 2 * n_act * ab + codes,                 # dy in, codes in, dx out
+        f"{w.norm.op}_bwd": 3 * n_norm * eb + 4 * rows,            # dz, z in, rstd in, dx out
+    }
+
+
+def source_hash():
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def load_traffic(kernel):
+    """HBM traffic of `kernel` from committed hardware-counter summaries, or None when
+    there is none or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{WORKLOAD}.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    if rec.get("source_sha256") != source_hash():
+        return None
+    return rec.get("traffic_bytes")
+
+
+def cpu_baseline(w, min_seconds=10.0):
+    """The CPU oracle, as it stands, on the whole step (every row of every tensor),
+    repeated until at least `min_seconds` of wall time; scaled to the same
+    algorithmic-bytes unit as the GPU value. NumPy runs these elementwise and
+    row-reduction ufuncs on one thread."""
+    import oracle
+    eps = float(np.float32(w.norm.eps))
+    x, dz, g, dy = w.norm_x(), w.norm_dz(), w.act_x(), w.act_dy()
+    dt_n, dt_a = w.norm.dtype, w.act.dtype
+    ofwd = {"msrms": oracle.msrms_fwd, "msln": oracle.msln_fwd}[w.norm.op]
+    obwd = {"msrms": oracle.msrms_bwd, "msln": oracle.msln_bwd}[w.norm.op]
+    afwd = {"resilu2": oracle.resilu2_fwd, "regelu2": oracle.regelu2_fwd}[w.act.op]
+    abwd = {"resilu2": oracle.resilu2_bwd, "regelu2": oracle.regelu2_bwd}[w.act.op]
+    passes = 0
+    t0 = time.perf_counter()
+    while True:
+        z, r = ofwd(oracle.decode(x, dt_n), eps)
+        z_s, r_s = oracle.encode(z, dt_n), r.astype(np.float32)
+        y, codes = afwd(oracle.decode(g, dt_a))
+        oracle.encode(y, dt_a)
+        oracle.encode(abwd(oracle.decode(dy, dt_a), codes), dt_a)
+        oracle.encode(obwd(oracle.decode(dz, dt_n), oracle.decode(z_s, dt_n), r_s), dt_n)
+        passes += 1
+        elapsed = time.perf_counter() - t0
+        if elapsed >= min_seconds:
+            break
+    step_bytes = sum(algorithmic_bytes(w).values())
+    return {
+        "value": round(passes * step_bytes / elapsed / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": (f"{passes} full pass(es) of the step (all {w.norm.rows} rows of every tensor), "
+                   f"fp64 NumPy, {elapsed:.2f} s wall"),
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU: the hot path is row- and element-local and runs "
+              f"per GPU with no communication, so --gpus {args.gpus} is not supported.",
+              file=sys.stderr)
+        sys.exit(2)
+    if args.steps < 1 or args.warmup < 0:
+        sys.exit("--steps must be >= 1 and --warmup >= 0")
+
+    import torch
+    import paper_2406_16282_amd as lmbp
+    from paper_2406_16282_amd import inputs
+
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    w = inputs.WORKLOADS[WORKLOAD]
+    nb = algorithmic_bytes(w)
+    eps = float(np.float32(w.norm.eps))
+    print(f"[bench] generating {WORKLOAD} inputs", file=sys.stderr, flush=True)
+    T = lambda a: inputs.storage_to_torch(a, dev)
+    x, dz, g, dy = T(w.norm_x()), T(w.norm_dz()), T(w.act_x()), T(w.act_dy())
+    z = torch.empty_like(x)
+    rstd = torch.empty(w.norm.rows, dtype=torch.float32, device=dev)
+    h = torch.empty_like(g)
+    codes = torch.empty(lmbp.codes_words(g.numel()), dtype=torch.int32, device=dev)
+    dg = torch.empty_like(dy)
+    dx = torch.empty_like(dz)
+    nfwd = {"msrms": lmbp.msrms_fwd, "msln": lmbp.msln_fwd}[w.norm.op]
+    nbwd = {"msrms": lmbp.msrms_bwd, "msln": lmbp.msln_bwd}[w.norm.op]
+    afwd = {"resilu2": lmbp.resilu2_fwd, "regelu2": lmbp.regelu2_fwd}[w.act.op]
+    abwd = {"resilu2": lmbp.resilu2_bwd, "regelu2": lmbp.regelu2_bwd}[w.act.op]
+    stream = torch.cuda.current_stream(dev)
+    names = list(nb.keys())
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        nfwd(x, eps, z=z, rstd=rstd, stream=stream)
+        if ev is not None:
+            ev[1].record(stream)
+        afwd(g, y=h, codes=codes, stream=stream)
+        if ev is not None:
+            ev[2].record(stream)
+        abwd(dy, codes, dx=dg, stream=stream)
+        if ev is not None:
+            ev[3].record(stream)
+        nbwd(dz, z, rstd, dx=dx, stream=stream)
+        if ev is not None:
+            ev[4].record(stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    print(f"[bench] warmup {args.warmup} steps done; timing {args.steps}", file=sys.stderr, flush=True)
+
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    evs = [[mk() for _ in range(5)] for _ in range(args.steps)]
+    start, end = mk(), mk()
+    torch.cuda.synchronize()
+    t_wall0 = time.perf_counter()
+    start.record(stream)
+    for k in range(args.steps):
+        step(evs[k])
+    end.record(stream)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter() - t_wall0
+
+    ms_total = start.elapsed_time(end)
+    ms_step = ms_total / args.steps
+    per_kernel_ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
+                     for i, n in enumerate(names)}
+    bytes_step = sum(nb.values())
+    value = bytes_step / (ms_step * 1e-3) / 1e9
+    per_kernel = {n: {"us": round(per_kernel_ms[n] * 1e3, 2),
+                      "bytes": nb[n],
+                      "GBps": round(nb[n] / (per_kernel_ms[n] * 1e-3) / 1e9, 1)}
+                  for n in names}
+    dominant = max(names, key=lambda n: per_kernel_ms[n])
+    achieved = nb[dominant] / (per_kernel_ms[dominant] * 1e-3) / 1e9
+    n_act = w.act.rows * w.act.cols
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": WORKLOAD,
+            "storage": w.act.dtype,
+            "norm": f"{w.norm.op} [{w.norm.rows}x{w.norm.cols}] eps={w.norm.eps:g}",
+            "act": f"{w.act.op} [{w.act.rows}x{w.act.cols}]",
+            "bytes_per_step": bytes_step,
+            "elements_per_step": 2 * (n_act + w.norm.rows * w.norm.cols),
+        },
+        "pct_of_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 1),
+        "elements_per_s": round(2 * (n_act + w.norm.rows * w.norm.cols) / (ms_step * 1e-3), 1),
+        "saved_bytes_per_elt": {
+            w.act.op: lmbp.codes_bytes(n_act) / n_act,
+            w.norm.op: 4.0 / w.norm.cols,
+            f"{w.act.op}_dense_reference": 2.0 if w.act.dtype == "bf16" else 4.0,
+        },
+        "per_kernel": per_kernel,
+        "roofline": {
+            "kernel": dominant,
+            "bound": "hbm",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": load_traffic(dominant),
+        },
+        "wall_s_timed": round(t_wall, 4),
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        out["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,131 @@
+/*
+ * lmbp.h - C ABI of the low-memory backpropagation kernels for AMD MI355X (gfx950).
+ *
+ * Eight operations from "Reducing Fine-Tuning Memory Overhead by Approximate and
+ * Memory-Sharing Backpropagation" (Yang et al., ICML 2024):
+ *
+ *   regelu2_fwd / regelu2_bwd   ReGELU2  (Sec. 4.2; constants Appendix E)
+ *   resilu2_fwd / resilu2_bwd   ReSiLU2  (Sec. 4.2; constants Appendix E)
+ *   msln_fwd    / msln_bwd      MS-LN    (Sec. 5.2 Alg. 1; Appendix G Alg. 2)
+ *   msrms_fwd   / msrms_bwd     MS-RMSNorm (Appendix G Alg. 3)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers are device pointers (HBM) owned and allocated by the caller; the
+ *   library never allocates, frees or synchronizes. Every call only enqueues
+ *   kernels on `stream` (a hipStream_t; NULL means the null stream) and returns.
+ * - Tensors are dense and row-major. Activation ops see a flat tensor of n
+ *   elements; norm ops see `rows` rows of `cols` elements (cols = the normalized
+ *   width p of the paper).
+ * - dtype selects the storage of every floating-point tensor argument except the
+ *   norm statistic `rstd`, which is always fp32. Arithmetic is fp32 in all cases.
+ * - Pointers need only element alignment (2 bytes for bf16, 4 for fp32 and for
+ *   codes / rstd); 16-byte aligned tensors whose rows are multiples of 16 bytes
+ *   take the vectorized path, anything else a slower general path with the same
+ *   results up to floating-point summation order.
+ * - Aliasing: only the exact in-place pairs named for each call are allowed
+ *   (same start address, same size). Any other overlap of two buffers of a call
+ *   returns LMBP_EOVERLAP before anything is launched.
+ * - Errors are checked on the host before any launch: LMBP_EINVAL for negative
+ *   sizes, cols == 0 with rows > 0, a NULL pointer with a nonzero size, a
+ *   misaligned pointer, or eps not finite and > 0; LMBP_EDTYPE for an unknown
+ *   dtype. n == 0 or rows == 0 is a successful no-op. LMBP_EHIP means the kernel
+ *   launch failed; lmbp_last_hip_error() then returns the hipError_t value for the
+ *   calling thread. No C++ exception crosses this interface.
+ * - Results are deterministic: no atomics, fixed reduction order.
+ */
+#ifndef LMBP_H
+#define LMBP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum { LMBP_FP32 = 0, LMBP_BF16 = 1 } lmbp_dtype;
+
+typedef enum {
+  LMBP_OK = 0,
+  LMBP_EINVAL = 1,
+  LMBP_EDTYPE = 2,
+  LMBP_EOVERLAP = 3,
+  LMBP_EHIP = 4
+} lmbp_status;
+
+/* Bytes of the packed code buffer for n activation elements: 4 * ceil(n / 16).
+ * The code of flat element i occupies bits [2(i mod 16), 2(i mod 16) + 1] of 32-bit
+ * word i / 16 (least significant bits first); unused bits of the last word are 0.
+ * Returns 0 for n <= 0. */
+size_t lmbp_codes_bytes(int64_t n);
+
+/* Static description of a status code. */
+const char *lmbp_strerror(lmbp_status st);
+
+/* hipError_t recorded by the last call on this thread that returned LMBP_EHIP. */
+int lmbp_last_hip_error(void);
+
+/* ------------------------------------------------------------------------
+ * ReGELU2 / ReSiLU2 (Sec. 4.2, eq. relus_family with k = 2).
+ *
+ * Forward: y = GELU(x) = x/2 (1 + erf(x / sqrt 2))   (regelu2)
+ *          y = SiLU(x) = x / (1 + e^-x)              (resilu2)
+ * computed exactly (fp32 arithmetic), plus the 2-bit code of every element: the
+ * number of the three biases c1 < c2 < c3 of Appendix E lying strictly below x.
+ * Backward: dx = dy * s[code], where s = (0, a1, a1 + a2, 1) is the slope of the
+ * three-ReLU combination on each of its four segments (Prop. 4.3).
+ *
+ *   x, y   : n elements of dtype. y == x (in place) is allowed.
+ *   codes  : lmbp_codes_bytes(n) bytes, 4-byte aligned, written completely
+ *            (including zero tail bits); must not overlap x or y.
+ *   dy, dx : n elements of dtype. dx == dy is allowed.
+ *   codes (bwd): as written by the matching forward; read only.
+ * ------------------------------------------------------------------------ */
+lmbp_status regelu2_fwd(lmbp_dtype dt, int64_t n, const void *x, void *y,
+                        uint32_t *codes, void *stream);
+lmbp_status regelu2_bwd(lmbp_dtype dt, int64_t n, const void *dy,
+                        const uint32_t *codes, void *dx, void *stream);
+lmbp_status resilu2_fwd(lmbp_dtype dt, int64_t n, const void *x, void *y,
+                        uint32_t *codes, void *stream);
+lmbp_status resilu2_bwd(lmbp_dtype dt, int64_t n, const void *dy,
+                        const uint32_t *codes, void *dx, void *stream);
+
+/* ------------------------------------------------------------------------
+ * MS-LN (Sec. 5.2 Alg. 1, Appendix G Alg. 2) and MS-RMSNorm (Alg. 3), for a
+ * norm whose affine (alpha, beta) has been merged into the following linear
+ * layer (W~ = W diag(alpha), b~ = W beta + b). Per row x of width p = cols:
+ *
+ * Forward:  sigma = sqrt(p^-1 |H x|^2 + eps),  z = H x / sigma,  rstd = 1 / sigma,
+ *           with H x = x - mean(x) for MS-LN and H x = x for MS-RMSNorm.
+ * Backward: dx = rstd * (H dz - z * mean(z * dz))   (= sigma^-1 (H - p^-1 z z^T) dz),
+ *           computed from the saved output z and rstd only.
+ *
+ *   x, z    : rows x cols of dtype. z == x (in place) is allowed. z is the
+ *             tensor the next (merged) linear layer keeps anyway.
+ *   rstd    : rows fp32 values; must not overlap x, z, dz or dx.
+ *   eps     : finite, > 0 (the paper uses 1e-6 or 1e-8; LLaMA-style RMSNorm 1e-5).
+ *   dz, dx  : rows x cols of dtype. dx == dz is allowed; dx must not overlap z.
+ * ------------------------------------------------------------------------ */
+lmbp_status msln_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps,
+                     const void *x, void *z, float *rstd, void *stream);
+lmbp_status msln_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void *dz,
+                     const void *z, const float *rstd, void *dx, void *stream);
+lmbp_status msrms_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps,
+                      const void *x, void *z, float *rstd, void *stream);
+lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void *dz,
+                      const void *z, const float *rstd, void *dx, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Measurement utility (not part of the method): copies `bytes` bytes from src
+ * to dst with 16-byte vector loads and stores. src and dst must be 16-byte
+ * aligned and must not overlap. Used as the plain-copy reference for bandwidth
+ * and hardware-counter calibration.
+ * ------------------------------------------------------------------------ */
+lmbp_status lmbp_copy(const void *src, void *dst, int64_t bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LMBP_H */

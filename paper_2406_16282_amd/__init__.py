@@ -1,0 +1,27 @@
+"""lmbp: MI355X (gfx950) HIP kernels for the hot path of Approximate and
+Memory-Sharing Backpropagation (Yang et al., ICML 2024).
+
+ReGELU2 / ReSiLU2 keep the exact activation in the forward pass and save only a
+2-bit segment code per element for a step-function derivative in the backward
+pass (Sec. 4.2). MS-LN / MS-RMSNorm, with the affine merged into the next linear
+layer, save only their output and one fp32 statistic per row (Sec. 5.2).
+
+The kernels live in liblmbp.so (C ABI in include/lmbp.h); ``binding`` marshals
+torch tensors into it. The library is loaded on first use.
+"""
+
+from .binding import (  # noqa: F401
+    LmbpError,
+    codes_bytes,
+    codes_words,
+    copy_bytes,
+    lib,
+    msln_bwd,
+    msln_fwd,
+    msrms_bwd,
+    msrms_fwd,
+    regelu2_bwd,
+    regelu2_fwd,
+    resilu2_bwd,
+    resilu2_fwd,
+)

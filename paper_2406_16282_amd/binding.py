@@ -1,0 +1,246 @@
+"""Thin ctypes binding of liblmbp (include/lmbp.h).
+
+Argument marshalling only: tensors are checked for device, dtype, size and
+contiguity, their device pointers and the current HIP stream are passed to the C
+ABI, and a non-OK status raises ``LmbpError``. Every step of the computation runs
+in the library's HIP kernels. There is no fallback: if liblmbp.so has not been
+built, the first call raises.
+"""
+
+import ctypes
+import os
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "liblmbp.so")
+
+FP32, BF16 = 0, 1
+OK, EINVAL, EDTYPE, EOVERLAP, EHIP = 0, 1, 2, 3, 4
+
+ACT_OPS = ("regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd")
+NORM_OPS = ("msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd")
+
+
+class LmbpError(RuntimeError):
+    def __init__(self, op, status, message):
+        super().__init__(f"{op}: status {status}: {message}")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load liblmbp.so (once) and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(
+            f"{LIB_PATH} is missing: build it with `python -c 'import __graft_entry__ as g; g.build()'`"
+            " (the HIP kernels are the only implementation)")
+    L = ctypes.CDLL(LIB_PATH)
+    i32, i64, f32, vp = ctypes.c_int, ctypes.c_int64, ctypes.c_float, ctypes.c_void_p
+    L.lmbp_codes_bytes.argtypes = [i64]
+    L.lmbp_codes_bytes.restype = ctypes.c_size_t
+    L.lmbp_strerror.argtypes = [i32]
+    L.lmbp_strerror.restype = ctypes.c_char_p
+    L.lmbp_last_hip_error.argtypes = []
+    L.lmbp_last_hip_error.restype = i32
+    for name in ACT_OPS:
+        fn = getattr(L, name)
+        fn.argtypes = [i32, i64, vp, vp, vp, vp]
+        fn.restype = i32
+    for name in ("msln_fwd", "msrms_fwd"):
+        fn = getattr(L, name)
+        fn.argtypes = [i32, i64, i64, f32, vp, vp, vp, vp]
+        fn.restype = i32
+    for name in ("msln_bwd", "msrms_bwd"):
+        fn = getattr(L, name)
+        fn.argtypes = [i32, i64, i64, vp, vp, vp, vp, vp]
+        fn.restype = i32
+    L.lmbp_copy.argtypes = [vp, vp, i64, vp]
+    L.lmbp_copy.restype = i32
+    _lib = L
+    return L
+
+
+def strerror(status):
+    return lib().lmbp_strerror(int(status)).decode()
+
+
+def codes_bytes(n):
+    return int(lib().lmbp_codes_bytes(int(n)))
+
+
+def codes_words(n):
+    return codes_bytes(n) // 4
+
+
+def _check(op, status):
+    if status != OK:
+        msg = strerror(status)
+        if status == EHIP:
+            msg += f" (hipError {lib().lmbp_last_hip_error()})"
+        raise LmbpError(op, status, msg)
+
+
+def _dtype_code(t):
+    if t.dtype == torch.float32:
+        return FP32
+    if t.dtype == torch.bfloat16:
+        return BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; expected float32 or bfloat16")
+
+
+def _dev(t, what):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{what} must be a torch.Tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{what} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{what} must be contiguous")
+    return t
+
+
+def _stream(t, stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _like(t, out, what):
+    if out is None:
+        return torch.empty_like(t)
+    _dev(out, what)
+    if out.dtype != t.dtype or out.numel() != t.numel() or out.device != t.device:
+        raise ValueError(f"{what} must match the input's dtype, size and device")
+    return out
+
+
+def _codes_out(n, device, codes):
+    words = codes_words(n)
+    if codes is None:
+        return torch.empty(words, dtype=torch.int32, device=device)
+    _dev(codes, "codes")
+    if codes.dtype != torch.int32 or codes.numel() < words or codes.device != device:
+        raise ValueError(f"codes must be an int32 GPU tensor of at least {words} words")
+    return codes
+
+
+def _act_fwd(op, x, y, codes, stream):
+    _dev(x, "x")
+    dt = _dtype_code(x)
+    y = _like(x, y, "y")
+    codes = _codes_out(x.numel(), x.device, codes)
+    _check(op, getattr(lib(), op)(dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes), _stream(x, stream)))
+    return y, codes
+
+
+def _act_bwd(op, dy, codes, dx, stream):
+    _dev(dy, "dy")
+    dt = _dtype_code(dy)
+    _dev(codes, "codes")
+    if codes.dtype != torch.int32 or codes.numel() < codes_words(dy.numel()):
+        raise ValueError("codes must be the int32 buffer written by the forward")
+    dx = _like(dy, dx, "dx")
+    _check(op, getattr(lib(), op)(dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx), _stream(dy, stream)))
+    return dx
+
+
+def regelu2_fwd(x, y=None, codes=None, stream=None):
+    """ReGELU2 forward: returns (GELU(x), packed 2-bit codes as int32 words)."""
+    return _act_fwd("regelu2_fwd", x, y, codes, stream)
+
+
+def regelu2_bwd(dy, codes, dx=None, stream=None):
+    """ReGELU2 backward: dx = dy * step derivative selected by the codes."""
+    return _act_bwd("regelu2_bwd", dy, codes, dx, stream)
+
+
+def resilu2_fwd(x, y=None, codes=None, stream=None):
+    """ReSiLU2 forward: returns (SiLU(x), packed 2-bit codes as int32 words)."""
+    return _act_fwd("resilu2_fwd", x, y, codes, stream)
+
+
+def resilu2_bwd(dy, codes, dx=None, stream=None):
+    """ReSiLU2 backward: dx = dy * step derivative selected by the codes."""
+    return _act_bwd("resilu2_bwd", dy, codes, dx, stream)
+
+
+def _rows_cols(t):
+    if t.dim() == 0:
+        raise ValueError("norm input needs at least one dimension")
+    cols = t.shape[-1]
+    rows = t.numel() // cols if cols else 0
+    return rows, cols
+
+
+def _norm_fwd(op, x, eps, z, rstd, stream):
+    _dev(x, "x")
+    dt = _dtype_code(x)
+    rows, cols = _rows_cols(x)
+    z = _like(x, z, "z")
+    if rstd is None:
+        rstd = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
+    else:
+        _dev(rstd, "rstd")
+        if rstd.dtype != torch.float32 or rstd.numel() != rows:
+            raise ValueError("rstd must be float32 with one value per row")
+    _check(op, getattr(lib(), op)(dt, rows, cols, float(eps), _ptr(x), _ptr(z), _ptr(rstd),
+                                  _stream(x, stream)))
+    return z, rstd
+
+
+def _norm_bwd(op, dz, z, rstd, dx, stream):
+    _dev(dz, "dz")
+    _dev(z, "z")
+    _dev(rstd, "rstd")
+    dt = _dtype_code(dz)
+    if z.dtype != dz.dtype or z.shape != dz.shape:
+        raise ValueError("z must match dz in dtype and shape")
+    rows, cols = _rows_cols(dz)
+    if rstd.dtype != torch.float32 or rstd.numel() != rows:
+        raise ValueError("rstd must be float32 with one value per row")
+    dx = _like(dz, dx, "dx")
+    _check(op, getattr(lib(), op)(dt, rows, cols, _ptr(dz), _ptr(z), _ptr(rstd), _ptr(dx),
+                                  _stream(dz, stream)))
+    return dx
+
+
+def msln_fwd(x, eps, z=None, rstd=None, stream=None):
+    """MS-LN forward over the last dimension: returns (z, rstd)."""
+    return _norm_fwd("msln_fwd", x, eps, z, rstd, stream)
+
+
+def msln_bwd(dz, z, rstd, dx=None, stream=None):
+    """MS-LN backward from the saved output z and rstd."""
+    return _norm_bwd("msln_bwd", dz, z, rstd, dx, stream)
+
+
+def msrms_fwd(x, eps, z=None, rstd=None, stream=None):
+    """MS-RMSNorm forward over the last dimension: returns (z, rstd)."""
+    return _norm_fwd("msrms_fwd", x, eps, z, rstd, stream)
+
+
+def msrms_bwd(dz, z, rstd, dx=None, stream=None):
+    """MS-RMSNorm backward from the saved output z and rstd."""
+    return _norm_bwd("msrms_bwd", dz, z, rstd, dx, stream)
+
+
+def copy_bytes(src, dst, stream=None):
+    """Measurement utility: 16-byte vector copy of src into dst (same byte size)."""
+    _dev(src, "src")
+    _dev(dst, "dst")
+    nbytes = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != nbytes:
+        raise ValueError("src and dst must have the same byte size")
+    _check("lmbp_copy", lib().lmbp_copy(_ptr(src), _ptr(dst), nbytes, _stream(src, stream)))
+    return dst

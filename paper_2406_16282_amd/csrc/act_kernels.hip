@@ -1,0 +1,337 @@
+// ReGELU2 / ReSiLU2 kernels for gfx950 (Sec. 4.2, eq. relus_family with k = 2;
+// constants from Appendix E).
+//
+// Forward: y = GELU(x) or SiLU(x) (exact function, fp32 arithmetic) and a 2-bit
+// segment code per element, packed 16 codes per 32-bit word, least significant
+// bits first. Backward: dx = dy * slope[code], slope = (0, a1, a1 + a2, 1).
+//
+// Layout of one wave's tile (fast path): lane l holds vectors j = 0..VPL-1 at
+// vector index tile_vec + j*64 + l, so every load and store instruction of the
+// wave covers 1 KiB of contiguous memory. A vector carries 4 (fp32) or 8 (bf16)
+// elements, i.e. 8 or 16 code bits; G = 4 or 2 neighbouring lanes hold the parts
+// of one code word. Each lane packs its G parts for G consecutive vectors into one
+// 32-bit value and the group transposes them with DPP quad permutes, after which
+// lane q of a group owns the complete word of vector (G*m + q): the word stores of
+// a wave are then contiguous too.
+#include "lmbp_device.hpp"
+#include "gelu_poly.h"
+#include "lmbp_launch.hpp"
+
+#include <type_traits>
+
+namespace lmbp {
+
+// ------------------------------------------------------------------ constants
+// Appendix E: weights a* and biases c* of the three-ReLU combinations.
+struct GeluConsts {
+  static constexpr double a1 = -0.04922261145617846;
+  static constexpr double a2 = 1.0979632065417297;
+  static constexpr double c1 = -3.1858810036855245;
+  static constexpr double c2 = -0.001178821281161997;
+  static constexpr double c3 = 3.190832613414926;
+};
+struct SiluConsts {
+  static constexpr double a1 = -0.04060357190528599;
+  static constexpr double a2 = 1.080925428529668;
+  static constexpr double c1 = -6.3050461001646445;
+  static constexpr double c2 = -0.0008684942046214787;
+  static constexpr double c3 = 6.325815242089708;
+};
+
+constexpr float f32_step(float f, int dir) {  // one ulp toward +inf (dir>0) or -inf
+  uint32_t b = __builtin_bit_cast(uint32_t, f);
+  const bool neg = (b >> 31) != 0u;
+  b = ((dir > 0) != neg) ? b + 1u : b - 1u;
+  return __builtin_bit_cast(float, b);
+}
+constexpr float round_down_f32(double c) {
+  const float f = static_cast<float>(c);
+  return (static_cast<double>(f) > c) ? f32_step(f, -1) : f;
+}
+
+// The code compares in fp32: for any fp32 (or bf16) value x and a bias c that is
+// not representable in fp32, x > c holds exactly when x > RD(c), RD(c) being the
+// largest fp32 value below c. The static_asserts check non-representability, so
+// the comparison is exact and no tie rule is ever needed.
+template <class C>
+struct Act {
+  static constexpr float t1 = round_down_f32(C::c1);
+  static constexpr float t2 = round_down_f32(C::c2);
+  static constexpr float t3 = round_down_f32(C::c3);
+  static_assert(static_cast<double>(t1) < C::c1 && C::c1 < static_cast<double>(f32_step(t1, 1)), "c1");
+  static_assert(static_cast<double>(t2) < C::c2 && C::c2 < static_cast<double>(f32_step(t2, 1)), "c2");
+  static_assert(static_cast<double>(t3) < C::c3 && C::c3 < static_cast<double>(f32_step(t3, 1)), "c3");
+  // Slopes of the combination on segments 1 and 2 (segment 0: 0, segment 3: 1).
+  static constexpr float s1 = static_cast<float>(C::a1);
+  static constexpr float s2 = static_cast<float>(C::a1 + C::a2);
+};
+using GeluAct = Act<GeluConsts>;
+using SiluAct = Act<SiluConsts>;
+
+template <class A>
+__device__ inline uint32_t seg_code(float x) {
+  // code = [x > c1] + [x > c2] + [x > c3] for c1 < c2 < c3, written as its two bits:
+  // bit 1 = [x > c2], bit 0 = [x > c1] xor [x > c2] xor [x > c3].
+  const uint32_t b1 = x > A::t2;
+  const uint32_t b0 = uint32_t(x > A::t1) ^ b1 ^ uint32_t(x > A::t3);
+  return b0 | (b1 << 1);
+}
+
+template <class A>
+__device__ inline float seg_slope(uint32_t c) {
+  return (c & 2u) ? ((c & 1u) ? 1.0f : A::s2) : ((c & 1u) ? A::s1 : 0.0f);
+}
+
+// ------------------------------------------------------------- activations
+// exp2 on the hardware unit (v_exp_f32); arguments here are never NaN.
+__device__ inline float hw_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
+__device__ inline float hw_rcp(float v) { return __builtin_amdgcn_rcpf(v); }
+
+// GELU(x) = x Phi(x). With t = |x| and Q(t) = 1 - Phi(t) = 2^E(t),
+// E(t) = -(log2 e / 2) t^2 + R(t), where R is the fitted polynomial of
+// gelu_poly.h (argument clamped to [0, T]). Phi(x) = Q(t) for x < 0 and 1 - Q(t)
+// otherwise.
+//   PRECISE (fp32 storage): degree-12 R; the quadratic term is carried in two
+//   pieces and the exponent split into integer and fraction so that no rounding
+//   of the large exponent reaches the result (relative error below 1e-6).
+//   Otherwise (bf16 storage): degree-8 R, single-piece exponent (about 1e-5).
+constexpr double kLog2eHalf = 0.72134752044448170368;  // log2(e) / 2
+constexpr float kLog2eHalfHi = static_cast<float>(kLog2eHalf);
+constexpr float kLog2eHalfLo = static_cast<float>(kLog2eHalf - static_cast<double>(kLog2eHalfHi));
+
+template <int D>
+__device__ inline float horner(const float (&c)[D], float v) {
+  float r = c[0];
+#pragma unroll
+  for (int k = 1; k < D; ++k) r = __builtin_fmaf(r, v, c[k]);
+  return r;
+}
+
+template <bool PRECISE>
+__device__ inline float gelu_f(float x) {
+  const float t = __builtin_fabsf(x);
+  const float v = __builtin_fmaf(__builtin_fminf(t, LMBP_GELU_T), LMBP_GELU_2_OVER_T, -1.0f);
+  float q;
+  if constexpr (PRECISE) {
+    const float r = horner(kGeluR12, v);
+    const float a_hi = t * -kLog2eHalfHi;
+    const float a_lo = __builtin_fmaf(t, -kLog2eHalfLo, __builtin_fmaf(t, -kLog2eHalfHi, -a_hi));
+    const float e0 = __builtin_fmaxf(__builtin_fmaf(t, a_hi, r), -256.0f);
+    const float k = __builtin_rintf(e0);
+    const float f = __builtin_fmaf(t, a_hi, -k) + __builtin_fmaf(t, a_lo, r);
+    q = __builtin_ldexpf(hw_exp2(f), int(k));
+  } else {
+    const float r = horner(kGeluR8, v);
+    q = hw_exp2(__builtin_fmaf(t, t * -kLog2eHalfHi, r));
+  }
+  const float phi = (x < 0.0f) ? q : 1.0f - q;
+  return x * phi;
+}
+
+// SiLU(x) = x / (1 + 2^(-x log2 e)).
+//   PRECISE: the exponent's rounding error is carried separately and applied as a
+//   first-order factor (1 + err ln 2) (product form, so an infinite 2^a stays inf).
+constexpr double kLog2e = 1.44269504088896340736;
+constexpr float kLog2eHi = static_cast<float>(kLog2e);
+constexpr float kLog2eLo = static_cast<float>(kLog2e - static_cast<double>(kLog2eHi));
+constexpr float kLn2 = 0.69314718055994530942f;
+
+template <bool PRECISE>
+__device__ inline float silu_f(float x) {
+  const float a = x * -kLog2eHi;
+  float e = hw_exp2(a);
+  if constexpr (PRECISE) {
+    const float a_lo = __builtin_fmaf(x, -kLog2eLo, __builtin_fmaf(x, -kLog2eHi, -a));
+    e = e * __builtin_fmaf(a_lo, kLn2, 1.0f);
+  }
+  return x * hw_rcp(1.0f + e);
+}
+
+template <int ACT, bool PRECISE>
+__device__ inline float act_value(float x) {
+  if constexpr (ACT == kGelu) return gelu_f<PRECISE>(x);
+  else return silu_f<PRECISE>(x);
+}
+
+template <int ACT>
+using ActOf = typename std::conditional<ACT == kGelu, GeluAct, SiluAct>::type;
+
+// -------------------------------------------------------------------- kernels
+template <class IO, int ACT, int VPL>
+__global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
+                                                      uint32_t* __restrict__ codes,
+                                                      int64_t n, int vec_ok) {
+  using A = ActOf<ACT>;
+  constexpr bool kPrecise = std::is_same<IO, F32>::value;
+  constexpr int E = IO::kPerVec;      // elements per 16-byte vector
+  constexpr int G = 16 / E;           // lanes sharing one code word
+  constexpr int PART = 2 * E;         // code bits per vector
+  constexpr int TILE = kWave * VPL * E;
+  static_assert(VPL % G == 0, "VPL must be a multiple of the lane group");
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  const int64_t base = wave * TILE;
+  if (base >= n) return;
+
+  if (vec_ok && base + TILE <= n) {
+    const int64_t vbase = base / E;
+    u32x4 in[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) in[j] = ldg16(x, vbase + j * kWave + lane);
+
+    uint32_t part[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      float f[E], o[E];
+      IO::unpack(in[j], f);
+      uint32_t p = 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        o[e] = act_value<ACT, kPrecise>(f[e]);
+        p |= seg_code<A>(f[e]) << (2 * e);
+      }
+      part[j] = p;
+      stg16(y, vbase + j * kWave + lane, IO::pack(o));
+    }
+
+    const int q = lane % G;
+    const int64_t wbase = base / 16;
+#pragma unroll
+    for (int m = 0; m < VPL / G; ++m) {
+      uint32_t packed = 0;
+#pragma unroll
+      for (int t = 0; t < G; ++t) packed |= part[G * m + t] << (t * PART);
+      // Step s: lane q sends part (q - s) mod G and receives, from lane (q + s) mod G,
+      // that lane's part for vector G*m + q.
+      uint32_t word = 0;
+#pragma unroll
+      for (int s = 0; s < G; ++s) {
+        const uint32_t send = __builtin_amdgcn_alignbit(packed, packed, uint32_t(((q - s + G) % G) * PART));
+        uint32_t recv;
+        if constexpr (G == 2) {
+          recv = (s == 0) ? send : group_rotate<2, 1>(send);
+        } else {
+          recv = (s == 0) ? send : (s == 1) ? group_rotate<4, 1>(send)
+               : (s == 2) ? group_rotate<4, 2>(send) : group_rotate<4, 3>(send);
+        }
+        const uint32_t mask = (PART == 32) ? 0xffffffffu : ((1u << PART) - 1u);
+        word |= (recv & mask) << (((q + s) % G) * PART);
+      }
+      codes[wbase + int64_t(G * m + q) * (kWave / G) + lane / G] = word;
+    }
+    return;
+  }
+
+  // General path: the partial last tile, or pointers that are not 16-byte aligned.
+  const int64_t end = (base + TILE < n) ? base + TILE : n;
+  const int64_t w_end = (end + 15) / 16;
+  for (int64_t w = base / 16 + lane; w < w_end; w += kWave) {
+    uint32_t word = 0;
+    for (int e = 0; e < 16; ++e) {
+      const int64_t i = w * 16 + e;
+      if (i < n) {
+        const float xv = IO::load1(x, i);
+        IO::store1(y, i, act_value<ACT, kPrecise>(xv));
+        word |= seg_code<A>(xv) << (2 * e);
+      }
+    }
+    codes[w] = word;
+  }
+}
+
+template <class IO, int ACT, int VPL>
+__global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
+                                                      const uint32_t* __restrict__ codes,
+                                                      void* dx, int64_t n, int vec_ok) {
+  using A = ActOf<ACT>;
+  constexpr int E = IO::kPerVec;
+  constexpr int G = 16 / E;
+  constexpr int PART = 2 * E;
+  constexpr int TILE = kWave * VPL * E;
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  const int64_t base = wave * TILE;
+  if (base >= n) return;
+
+  if (vec_ok && base + TILE <= n) {
+    const int64_t vbase = base / E;
+    const int64_t wbase = base / 16;
+    u32x4 in[VPL];
+    uint32_t word[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      in[j] = ldg16(dy, vbase + j * kWave + lane);
+      word[j] = codes[wbase + j * (kWave / G) + lane / G];
+    }
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      const uint32_t p = word[j] >> ((lane % G) * PART);
+      float f[E];
+      IO::unpack(in[j], f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) f[e] = f[e] * seg_slope<A>((p >> (2 * e)) & 3u);
+      stg16(dx, vbase + j * kWave + lane, IO::pack(f));
+    }
+    return;
+  }
+
+  const int64_t end = (base + TILE < n) ? base + TILE : n;
+  for (int64_t i = base + lane; i < end; i += kWave) {
+    const uint32_t c = (codes[i / 16] >> (2 * (i % 16))) & 3u;
+    IO::store1(dx, i, IO::load1(dy, i) * seg_slope<A>(c));
+  }
+}
+
+// ------------------------------------------------------------------ launchers
+namespace {
+constexpr int kActVPL = 4;
+template <class IO>
+constexpr int64_t act_tile() { return int64_t(kWave) * kActVPL * IO::kPerVec; }
+template <class IO>
+int64_t act_blocks(int64_t n) {
+  const int64_t waves = (n + act_tile<IO>() - 1) / act_tile<IO>();
+  return (waves + 3) / 4;
+}
+}  // namespace
+
+template <class IO, int ACT>
+hipError_t launch_act_fwd_t(int64_t n, const void* x, void* y, uint32_t* codes, bool vec_ok,
+                            hipStream_t s) {
+  const int64_t blocks = act_blocks<IO>(n);
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((act_fwd_kernel<IO, ACT, kActVPL>), dim3(unsigned(blocks)), dim3(256), 0, s,
+                     x, y, codes, n, int(vec_ok));
+  return hipGetLastError();
+}
+
+template <class IO, int ACT>
+hipError_t launch_act_bwd_t(int64_t n, const void* dy, const uint32_t* codes, void* dx,
+                            bool vec_ok, hipStream_t s) {
+  const int64_t blocks = act_blocks<IO>(n);
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((act_bwd_kernel<IO, ACT, kActVPL>), dim3(unsigned(blocks)), dim3(256), 0, s,
+                     dy, codes, dx, n, int(vec_ok));
+  return hipGetLastError();
+}
+
+hipError_t launch_act_fwd(int act, bool bf16, int64_t n, const void* x, void* y,
+                          uint32_t* codes, bool vec_ok, hipStream_t s) {
+  if (act == kGelu)
+    return bf16 ? launch_act_fwd_t<BF16, kGelu>(n, x, y, codes, vec_ok, s)
+                : launch_act_fwd_t<F32, kGelu>(n, x, y, codes, vec_ok, s);
+  return bf16 ? launch_act_fwd_t<BF16, kSilu>(n, x, y, codes, vec_ok, s)
+              : launch_act_fwd_t<F32, kSilu>(n, x, y, codes, vec_ok, s);
+}
+
+hipError_t launch_act_bwd(int act, bool bf16, int64_t n, const void* dy, const uint32_t* codes,
+                          void* dx, bool vec_ok, hipStream_t s) {
+  if (act == kGelu)
+    return bf16 ? launch_act_bwd_t<BF16, kGelu>(n, dy, codes, dx, vec_ok, s)
+                : launch_act_bwd_t<F32, kGelu>(n, dy, codes, dx, vec_ok, s);
+  return bf16 ? launch_act_bwd_t<BF16, kSilu>(n, dy, codes, dx, vec_ok, s)
+              : launch_act_bwd_t<F32, kSilu>(n, dy, codes, dx, vec_ok, s);
+}
+
+}  // namespace lmbp

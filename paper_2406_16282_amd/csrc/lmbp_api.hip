@@ -1,0 +1,184 @@
+// C ABI of liblmbp (declared in include/lmbp.h): host-side validation, path
+// selection and launch. Nothing here allocates, frees or synchronizes.
+#include "lmbp.h"
+#include "lmbp_launch.hpp"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+struct Span {
+  uintptr_t lo, hi;  // [lo, hi)
+};
+
+Span span(const void* p, uint64_t bytes) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+  return Span{a, a + bytes};
+}
+
+bool overlaps(Span a, Span b) {
+  return a.lo < b.hi && b.lo < a.hi && a.hi > a.lo && b.hi > b.lo;
+}
+
+// Two buffers of a call may either be disjoint or, when `same_ok`, identical.
+bool bad_pair(Span a, Span b, bool same_ok) {
+  if (!overlaps(a, b)) return false;
+  return !(same_ok && a.lo == b.lo && a.hi == b.hi);
+}
+
+bool aligned(const void* p, uintptr_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+int elem_bytes(lmbp_dtype dt) { return dt == LMBP_BF16 ? 2 : 4; }
+
+bool known_dtype(int dt) { return dt == LMBP_FP32 || dt == LMBP_BF16; }
+
+lmbp_status from_hip(hipError_t e) {
+  if (e == hipSuccess) return LMBP_OK;
+  g_last_hip_error = int(e);
+  return LMBP_EHIP;
+}
+
+lmbp_status act_fwd(int act, lmbp_dtype dt, int64_t n, const void* x, void* y, uint32_t* codes,
+                    void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (n < 0 || uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (n == 0) return LMBP_OK;
+  if (!x || !y || !codes) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(x, eb) || !aligned(y, eb) || !aligned(codes, 4)) return LMBP_EINVAL;
+  const Span sx = span(x, uint64_t(n) * eb), sy = span(y, uint64_t(n) * eb);
+  const Span sc = span(codes, lmbp_codes_bytes(n));
+  if (bad_pair(sx, sy, true) || bad_pair(sc, sx, false) || bad_pair(sc, sy, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(x, 16) && aligned(y, 16);
+  return from_hip(lmbp::launch_act_fwd(act, dt == LMBP_BF16, n, x, y, codes, vec_ok,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+lmbp_status act_bwd(int act, lmbp_dtype dt, int64_t n, const void* dy, const uint32_t* codes,
+                    void* dx, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (n < 0 || uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (n == 0) return LMBP_OK;
+  if (!dy || !dx || !codes) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(dy, eb) || !aligned(dx, eb) || !aligned(codes, 4)) return LMBP_EINVAL;
+  const Span sg = span(dy, uint64_t(n) * eb), sd = span(dx, uint64_t(n) * eb);
+  const Span sc = span(codes, lmbp_codes_bytes(n));
+  if (bad_pair(sg, sd, true) || bad_pair(sc, sg, false) || bad_pair(sc, sd, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(dy, 16) && aligned(dx, 16);
+  return from_hip(lmbp::launch_act_bwd(act, dt == LMBP_BF16, n, dy, codes, dx, vec_ok,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+lmbp_status norm_fwd(bool ln, lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x,
+                     void* z, float* rstd, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (rows < 0 || cols < 0) return LMBP_EINVAL;
+  if (rows == 0) return LMBP_OK;
+  if (cols == 0) return LMBP_EINVAL;
+  if (!(std::isfinite(eps) && eps > 0.0f)) return LMBP_EINVAL;
+  if (!x || !z || !rstd) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(x, eb) || !aligned(z, eb) || !aligned(rstd, 4)) return LMBP_EINVAL;
+  if (uint64_t(rows) > (uint64_t(1) << 62) / uint64_t(cols) / 4) return LMBP_EINVAL;
+  const uint64_t bytes = uint64_t(rows) * uint64_t(cols) * eb;
+  const Span sx = span(x, bytes), sz = span(z, bytes), sr = span(rstd, uint64_t(rows) * 4);
+  if (bad_pair(sx, sz, true) || bad_pair(sr, sx, false) || bad_pair(sr, sz, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(x, 16) && aligned(z, 16) && (uint64_t(cols) * eb) % 16 == 0;
+  return from_hip(lmbp::launch_norm_fwd(ln, dt == LMBP_BF16, rows, cols, eps, x, z, rstd, vec_ok,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+lmbp_status norm_bwd(bool ln, lmbp_dtype dt, int64_t rows, int64_t cols, const void* dz,
+                     const void* z, const float* rstd, void* dx, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (rows < 0 || cols < 0) return LMBP_EINVAL;
+  if (rows == 0) return LMBP_OK;
+  if (cols == 0) return LMBP_EINVAL;
+  if (!dz || !z || !rstd || !dx) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(dz, eb) || !aligned(z, eb) || !aligned(dx, eb) || !aligned(rstd, 4))
+    return LMBP_EINVAL;
+  if (uint64_t(rows) > (uint64_t(1) << 62) / uint64_t(cols) / 4) return LMBP_EINVAL;
+  const uint64_t bytes = uint64_t(rows) * uint64_t(cols) * eb;
+  const Span sg = span(dz, bytes), sz = span(z, bytes), sd = span(dx, bytes);
+  const Span sr = span(rstd, uint64_t(rows) * 4);
+  if (bad_pair(sg, sd, true) || bad_pair(sz, sd, false) || bad_pair(sr, sd, false) ||
+      bad_pair(sr, sg, false) || bad_pair(sr, sz, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(dz, 16) && aligned(z, 16) && aligned(dx, 16) &&
+                      (uint64_t(cols) * eb) % 16 == 0;
+  return from_hip(lmbp::launch_norm_bwd(ln, dt == LMBP_BF16, rows, cols, dz, z, rstd, dx, vec_ok,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace
+
+extern "C" {
+
+size_t lmbp_codes_bytes(int64_t n) { return n <= 0 ? 0 : size_t((uint64_t(n) + 15) / 16) * 4; }
+
+const char* lmbp_strerror(lmbp_status st) {
+  switch (st) {
+    case LMBP_OK: return "success";
+    case LMBP_EINVAL: return "invalid argument (size, pointer, alignment or eps)";
+    case LMBP_EDTYPE: return "unknown dtype";
+    case LMBP_EOVERLAP: return "buffers overlap in a way the call does not allow";
+    case LMBP_EHIP: return "HIP kernel launch failed";
+  }
+  return "unknown status";
+}
+
+int lmbp_last_hip_error(void) { return g_last_hip_error; }
+
+lmbp_status regelu2_fwd(lmbp_dtype dt, int64_t n, const void* x, void* y, uint32_t* codes,
+                        void* stream) {
+  return act_fwd(lmbp::kGelu, dt, n, x, y, codes, stream);
+}
+lmbp_status regelu2_bwd(lmbp_dtype dt, int64_t n, const void* dy, const uint32_t* codes, void* dx,
+                        void* stream) {
+  return act_bwd(lmbp::kGelu, dt, n, dy, codes, dx, stream);
+}
+lmbp_status resilu2_fwd(lmbp_dtype dt, int64_t n, const void* x, void* y, uint32_t* codes,
+                        void* stream) {
+  return act_fwd(lmbp::kSilu, dt, n, x, y, codes, stream);
+}
+lmbp_status resilu2_bwd(lmbp_dtype dt, int64_t n, const void* dy, const uint32_t* codes, void* dx,
+                        void* stream) {
+  return act_bwd(lmbp::kSilu, dt, n, dy, codes, dx, stream);
+}
+
+lmbp_status msln_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x, void* z,
+                     float* rstd, void* stream) {
+  return norm_fwd(true, dt, rows, cols, eps, x, z, rstd, stream);
+}
+lmbp_status msln_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void* dz, const void* z,
+                     const float* rstd, void* dx, void* stream) {
+  return norm_bwd(true, dt, rows, cols, dz, z, rstd, dx, stream);
+}
+lmbp_status msrms_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x, void* z,
+                      float* rstd, void* stream) {
+  return norm_fwd(false, dt, rows, cols, eps, x, z, rstd, stream);
+}
+lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void* dz, const void* z,
+                      const float* rstd, void* dx, void* stream) {
+  return norm_bwd(false, dt, rows, cols, dz, z, rstd, dx, stream);
+}
+
+lmbp_status lmbp_copy(const void* src, void* dst, int64_t bytes, void* stream) {
+  if (bytes < 0) return LMBP_EINVAL;
+  if (bytes == 0) return LMBP_OK;
+  if (!src || !dst || !aligned(src, 16) || !aligned(dst, 16)) return LMBP_EINVAL;
+  if (overlaps(span(src, uint64_t(bytes)), span(dst, uint64_t(bytes)))) return LMBP_EOVERLAP;
+  return from_hip(lmbp::launch_copy(src, dst, bytes, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

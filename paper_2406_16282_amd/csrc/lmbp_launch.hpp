@@ -1,0 +1,26 @@
+// Internal launcher declarations between the C ABI layer and the kernel files.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lmbp {
+
+enum { kGelu = 0, kSilu = 1 };
+
+hipError_t launch_act_fwd(int act, bool bf16, int64_t n, const void* x, void* y,
+                          uint32_t* codes, bool vec_ok, hipStream_t s);
+hipError_t launch_act_bwd(int act, bool bf16, int64_t n, const void* dy, const uint32_t* codes,
+                          void* dx, bool vec_ok, hipStream_t s);
+
+// vec_ok: every tensor pointer 16-byte aligned and cols * element bytes a
+// multiple of 16 (each row starts on a vector boundary).
+hipError_t launch_norm_fwd(bool ln, bool bf16, int64_t rows, int64_t cols, float eps,
+                           const void* x, void* z, float* rstd, bool vec_ok, hipStream_t s);
+hipError_t launch_norm_bwd(bool ln, bool bf16, int64_t rows, int64_t cols, const void* dz,
+                           const void* z, const float* rstd, void* dx, bool vec_ok,
+                           hipStream_t s);
+
+hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
+
+}  // namespace lmbp

@@ -1,0 +1,124 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared entry
+point, and rejects invalid calls on the host before any launch."""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2406_16282_amd as lmbp
+from paper_2406_16282_amd import binding as B
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lmbp.h")
+
+# Fake device addresses: every call below fails validation before anything is
+# launched or dereferenced.
+P = 0x7F0000000000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*([a-z_0-9]+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(B.LIB_PATH):
+        pytest.fail("liblmbp.so is not built; run __graft_entry__.build()")
+    return lmbp.lib()
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert set(B.ACT_OPS + B.NORM_OPS) <= set(names)
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_codes_bytes(L):
+    assert [L.lmbp_codes_bytes(n) for n in (-5, 0, 1, 15, 16, 17, 32, 33)] == [0, 0, 4, 4, 4, 8, 8, 12]
+    assert L.lmbp_codes_bytes(90177536) == 90177536 // 4
+
+
+def test_strerror(L):
+    for st in range(5):
+        assert len(B.strerror(st)) > 3
+    assert B.strerror(99) == "unknown status"
+
+
+@pytest.mark.parametrize("op", B.ACT_OPS)
+def test_activation_errors(L, op):
+    f = getattr(L, op)
+    s = None
+    assert f(7, 16, P, P + 4096, P + 8192, s) == B.EDTYPE
+    assert f(B.FP32, -1, P, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 0, P, P + 4096, P + 8192, s) == B.OK          # no-op
+    assert f(B.FP32, 0, None, None, None, s) == B.OK
+    assert f(B.FP32, 16, None, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 16, P, None, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 16, P, P + 4096, None, s) == B.EINVAL
+    assert f(B.FP32, 16, P + 2, P + 4096, P + 8192, s) == B.EINVAL  # not element aligned
+    assert f(B.BF16, 16, P + 1, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 16, P, P + 4096, P + 8194, s) == B.EINVAL     # codes not 4-byte aligned
+    assert f(B.FP32, 16, P, P + 32, P + 8192, s) == B.EOVERLAP     # partial overlap of tensors
+    assert f(B.FP32, 16, P, P + 4096, P + 60, s) == B.EOVERLAP     # codes inside the first tensor
+    assert f(B.FP32, 16, P, P + 4096, P + 4096, s) == B.EOVERLAP   # codes on the second tensor
+    assert f(B.FP32, 1 << 61, P, P + 4096, P + 8192, s) == B.EINVAL
+
+
+@pytest.mark.parametrize("op", ["msln_fwd", "msrms_fwd"])
+def test_norm_fwd_errors(L, op):
+    f = getattr(L, op)
+    s = None
+    assert f(9, 4, 8, 1e-5, P, P + 4096, P + 8192, s) == B.EDTYPE
+    assert f(B.FP32, -1, 8, 1e-5, P, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 4, -8, 1e-5, P, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 4, 0, 1e-5, P, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 0, 8, 1e-5, P, P + 4096, P + 8192, s) == B.OK
+    for eps in (0.0, -1e-5, math.inf, math.nan):
+        assert f(B.FP32, 4, 8, eps, P, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 4, 8, 1e-5, None, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 4, 8, 1e-5, P, P + 4096, P + 8194, s) == B.EINVAL  # rstd misaligned
+    assert f(B.BF16, 4, 8, 1e-5, P + 1, P + 4096, P + 8192, s) == B.EINVAL
+    assert f(B.FP32, 4, 8, 1e-5, P, P + 64, P + 8192, s) == B.EOVERLAP   # x/z partial overlap
+    assert f(B.FP32, 4, 8, 1e-5, P, P + 4096, P + 100, s) == B.EOVERLAP  # rstd inside x
+    assert f(B.FP32, 4, 8, 1e-5, P, P + 4096, P + 4096, s) == B.EOVERLAP # rstd on z
+
+
+@pytest.mark.parametrize("op", ["msln_bwd", "msrms_bwd"])
+def test_norm_bwd_errors(L, op):
+    f = getattr(L, op)
+    s = None
+    dz, z, r, dx = P, P + 4096, P + 8192, P + 12288
+    assert f(3, 4, 8, dz, z, r, dx, s) == B.EDTYPE
+    assert f(B.FP32, 4, 0, dz, z, r, dx, s) == B.EINVAL
+    assert f(B.FP32, 0, 8, dz, z, r, dx, s) == B.OK
+    assert f(B.FP32, 4, 8, dz, z, r, None, s) == B.EINVAL
+    assert f(B.FP32, 4, 8, dz, z, r + 2, dx, s) == B.EINVAL
+    assert f(B.FP32, 4, 8, dz, z, r, z, s) == B.EOVERLAP          # dx on z is not allowed
+    assert f(B.FP32, 4, 8, dz, z, r, dz + 4, s) == B.EOVERLAP     # partial overlap with dz
+    assert f(B.FP32, 4, 8, dz, z, dz + 16, dx, s) == B.EOVERLAP   # rstd inside dz
+
+
+def test_copy_errors(L):
+    assert L.lmbp_copy(P, P + 4096, -1, None) == B.EINVAL
+    assert L.lmbp_copy(P, P + 4096, 0, None) == B.OK
+    assert L.lmbp_copy(P + 8, P + 4096, 64, None) == B.EINVAL
+    assert L.lmbp_copy(P, P + 32, 64, None) == B.EOVERLAP
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(B, "_lib", None)
+    monkeypatch.setattr(B, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="missing"):
+        B.lib()
+
+
+def test_binding_rejects_cpu_tensors(L):
+    import torch
+    with pytest.raises(ValueError):
+        lmbp.resilu2_fwd(torch.zeros(16, dtype=torch.bfloat16))

@@ -1,0 +1,162 @@
+"""GPU parity of ReGELU2 / ReSiLU2 against the CPU oracle (codes bit-exact, floats
+under the rules in compare.py), through the C ABI."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2406_16282_amd as lmbp
+from paper_2406_16282_amd import inputs
+from compare import (assert_codes_equal, assert_mixed, assert_rel, bf16_ulp_distance,
+                     rtol_for)
+
+pytestmark = pytest.mark.gpu
+
+OPS = {
+    "regelu2": (lmbp.regelu2_fwd, lmbp.regelu2_bwd, oracle.regelu2_fwd, oracle.regelu2_bwd, oracle.GELU_C),
+    "resilu2": (lmbp.resilu2_fwd, lmbp.resilu2_bwd, oracle.resilu2_fwd, oracle.resilu2_bwd, oracle.SILU_C),
+}
+DEV = "cuda:0"
+
+
+def T(a):
+    return inputs.storage_to_torch(a, DEV)
+
+
+def H(t):
+    return inputs.torch_to_storage(t)
+
+
+def check_act(op, dtype, x, dy, label):
+    fwd, bwd, ofwd, obwd, _ = OPS[op]
+    print(f"[act] {label}: op={op} dtype={dtype} shape={x.shape}", flush=True)
+    rtol = rtol_for(dtype)
+    x64 = oracle.decode(x, dtype)
+    y_o, w_o = ofwd(x64)
+    dx_o = obwd(oracle.decode(dy, dtype), w_o)
+
+    y, codes = fwd(T(x))
+    dx = bwd(T(dy), T(w_o))          # backward fed the oracle's saved codes
+    torch.cuda.synchronize()
+
+    assert_codes_equal(H(codes), w_o, f"{label} codes")
+    y64 = oracle.decode(H(y), dtype)
+    dx64 = oracle.decode(H(dx), dtype)
+    shape2 = x.shape if x.ndim == 2 else (1, x.size)
+    assert_mixed(y64.reshape(shape2), y_o.reshape(shape2), rtol, f"{label} y")
+    assert_rel(y64, y_o, rtol, f"{label} y (strict)")
+    assert_mixed(dx64.reshape(shape2), dx_o.reshape(shape2), rtol, f"{label} dx")
+    assert_rel(dx64, dx_o, rtol, f"{label} dx (strict)", floor=0.0)
+    zero = oracle.unpack_codes(w_o, x.size).reshape(x.shape) == 0
+    assert np.all(dx64[zero] == 0.0), f"{label}: code-0 gradients must be exactly zero"
+    if dtype == "bf16":
+        # Stored bf16 values are the oracle's correctly rounded value or a neighbour
+        # (never more than one step off), and nearly always the value itself. Outputs
+        # below 2^-60 are excluded, as in the strict relative rule.
+        for got, ref, name in ((H(y), y_o, "y"), (H(dx), dx_o, "dx")):
+            m = np.abs(ref) >= 2.0 ** -60
+            d = bf16_ulp_distance(got, ref)[m]
+            assert d.max() <= 1 and np.mean(d == 0) >= 0.99, f"{label}: bf16 rounding of {name}"
+    return y, codes
+
+
+CASES = [
+    # (op, dtype, shape, x_std, dy_std)
+    ("regelu2", "fp32", (8 * 197, 3072), 1.0, 1.0),        # ViT-B fp32 block, full size
+    ("regelu2", "bf16", (1024, 3072), 1.5, 1e-2),           # ViT-B bf16 rows (subset)
+    ("resilu2", "bf16", (512, 11008), 2.0, 1e-3),           # LLaMA-7B gate rows (subset)
+    ("resilu2", "fp32", (300, 11008), 2.0, 1e-3),
+    ("regelu2", "bf16", (37, 1000), 3.0, 1.0),              # ragged: partial tile, n % 16 != 0
+    ("resilu2", "fp32", (1, 1), 1.0, 1.0),
+    ("regelu2", "fp32", (1, 17), 1.0, 1.0),
+    ("resilu2", "bf16", (3, 2049), 4.0, 1.0),
+    ("regelu2", "bf16", (1, 2048 * 5), 1.0, 1.0),           # exact multiple of the bf16 tile
+]
+
+
+@pytest.mark.parametrize("op,dtype,shape,xs,gs", CASES)
+def test_parity(op, dtype, shape, xs, gs):
+    x = inputs.normal(shape, xs, dtype, tensor_id=inputs.ACT_X)
+    dy = inputs.normal(shape, gs, dtype, tensor_id=inputs.ACT_DY)
+    check_act(op, dtype, x, dy, f"normal{shape}")
+
+
+@pytest.mark.parametrize("op", ["resilu2", "regelu2"])
+def test_outlier_mixture(op):
+    shape = (256, 13824)
+    x = inputs.outlier_mixture(shape, "bf16", tensor_id=inputs.ACT_X)
+    dy = inputs.normal(shape, 1e-3, "bf16", tensor_id=inputs.ACT_DY)
+    check_act(op, "bf16", x, dy, "mixture")
+
+
+@pytest.mark.parametrize("shape", inputs.EDGE_SHAPES)
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("op", ["regelu2", "resilu2"])
+def test_edge_values(op, dtype, shape):
+    """Threshold neighbours (+-3 ulps of every bias), +-1e4, log-uniform magnitudes,
+    signed zeros and subnormals; widths that are not multiples of 64."""
+    x = inputs.edge_activation(shape, dtype, OPS[op][4])
+    dy = inputs.normal(shape, 1.0, dtype, tensor_id=inputs.ACT_DY)
+    check_act(op, dtype, x, dy, f"edge{shape}")
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("op", ["regelu2", "resilu2"])
+def test_misaligned_base_pointer(op, dtype):
+    """Tensors starting one element past a 16-byte boundary take the general path."""
+    fwd, bwd, ofwd, obwd, _ = OPS[op]
+    n = 5 * 4096 + 3
+    x = inputs.normal((n + 1,), 2.0, dtype, tensor_id=inputs.ACT_X)
+    dy = inputs.normal((n + 1,), 1.0, dtype, tensor_id=inputs.ACT_DY)
+    xt, dyt = T(x), T(dy)
+    y_buf = torch.empty_like(xt)
+    dx_buf = torch.empty_like(dyt)
+    y, codes = fwd(xt[1:], y=y_buf[1:])
+    y_o, w_o = ofwd(oracle.decode(x[1:], dtype))
+    dx = bwd(dyt[1:], T(w_o), dx=dx_buf[1:])
+    torch.cuda.synchronize()
+    assert_codes_equal(H(codes), w_o, "misaligned codes")
+    rtol = rtol_for(dtype)
+    assert_rel(oracle.decode(H(y), dtype), y_o, rtol, "misaligned y")
+    assert_rel(oracle.decode(H(dx), dtype), obwd(oracle.decode(dy[1:], dtype), w_o), rtol,
+               "misaligned dx", floor=0.0)
+
+
+@pytest.mark.parametrize("op", ["regelu2", "resilu2"])
+def test_in_place_and_determinism(op):
+    fwd, bwd, ofwd, obwd, _ = OPS[op]
+    shape = (64, 11008)
+    x = inputs.normal(shape, 2.0, "bf16", tensor_id=inputs.ACT_X)
+    dy = inputs.normal(shape, 1e-3, "bf16", tensor_id=inputs.ACT_DY)
+    y1, c1 = fwd(T(x))
+    xt = T(x)
+    y2, c2 = fwd(xt, y=xt)                 # in place
+    dyt = T(dy)
+    dx1 = bwd(T(dy), c1)
+    dx2 = bwd(dyt, c1, dx=dyt)             # in place
+    y3, c3 = fwd(T(x))
+    torch.cuda.synchronize()
+    assert y2.data_ptr() == xt.data_ptr() and dx2.data_ptr() == dyt.data_ptr()
+    for a, b in ((y1, y2), (y1, y3), (c1, c2), (c1, c3), (dx1, dx2)):
+        assert np.array_equal(H(a), H(b))
+
+
+def test_empty_tensor_is_noop():
+    x = torch.empty(0, dtype=torch.bfloat16, device=DEV)
+    y, codes = lmbp.resilu2_fwd(x)
+    dx = lmbp.resilu2_bwd(x, codes)
+    assert y.numel() == 0 and codes.numel() == 0 and dx.numel() == 0
+
+
+def test_chained_fwd_bwd_regelu2_fp32():
+    """GPU forward then GPU backward on its own codes, against the oracle chain."""
+    shape = (8 * 197, 3072)
+    x = inputs.normal(shape, 1.0, "fp32", tensor_id=inputs.ACT_X)
+    dy = inputs.normal(shape, 1.0, "fp32", tensor_id=inputs.ACT_DY)
+    y, codes = lmbp.regelu2_fwd(T(x))
+    dx = lmbp.regelu2_bwd(T(dy), codes)
+    torch.cuda.synchronize()
+    y_o, w_o = oracle.regelu2_fwd(oracle.decode(x, "fp32"))
+    dx_o = oracle.regelu2_bwd(oracle.decode(dy, "fp32"), w_o)
+    assert_rel(oracle.decode(H(dx), "fp32"), dx_o, 1e-5, "chained dx", floor=0.0)
