@@ -10,8 +10,10 @@ workload (bf16 storage, fp32 arithmetic), in training order:
 
 Inputs are seeded synthetic tensors already resident in HBM. The reported value
 is the algorithmic HBM traffic of the step (bytes each kernel must read and
-write) divided by the measured step time. Per-kernel durations come from HIP
-events recorded on the stream the kernels run on, inside the timed region.
+write) divided by the measured step time (K steps back to back between two HIP
+events on the kernels' stream). Per-kernel launch durations come from a second
+event-timed loop that launches each kernel back to back over rotating tensor
+sets; the dominant kernel's figure feeds the roofline entry.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
 """
@@ -140,12 +142,6 @@ def main():
     print(f"[bench] generating {WORKLOAD} inputs", file=sys.stderr, flush=True)
     T = lambda a: inputs.storage_to_torch(a, dev)
     x, dz, g, dy = T(w.norm_x()), T(w.norm_dz()), T(w.act_x()), T(w.act_dy())
-    z = torch.empty_like(x)
-    rstd = torch.empty(w.norm.rows, dtype=torch.float32, device=dev)
-    h = torch.empty_like(g)
-    codes = torch.empty(lmbp.codes_words(g.numel()), dtype=torch.int32, device=dev)
-    dg = torch.empty_like(dy)
-    dx = torch.empty_like(dz)
     nfwd = {"msrms": lmbp.msrms_fwd, "msln": lmbp.msln_fwd}[w.norm.op]
     nbwd = {"msrms": lmbp.msrms_bwd, "msln": lmbp.msln_bwd}[w.norm.op]
     afwd = {"resilu2": lmbp.resilu2_fwd, "regelu2": lmbp.regelu2_fwd}[w.act.op]
@@ -153,43 +149,90 @@ def main():
     stream = torch.cuda.current_stream(dev)
     names = list(nb.keys())
 
-    def step(ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        nfwd(x, eps, z=z, rstd=rstd, stream=stream)
-        if ev is not None:
-            ev[1].record(stream)
-        afwd(g, y=h, codes=codes, stream=stream)
-        if ev is not None:
-            ev[2].record(stream)
-        abwd(dy, codes, dx=dg, stream=stream)
-        if ev is not None:
-            ev[3].record(stream)
-        nbwd(dz, z, rstd, dx=dx, stream=stream)
-        if ev is not None:
-            ev[4].record(stream)
+    class Set:
+        """One full set of step tensors (inputs and saved state / outputs)."""
+        def __init__(self, x, dz, g, dy):
+            self.x, self.dz, self.g, self.dy = x, dz, g, dy
+            self.z = torch.empty_like(x)
+            self.rstd = torch.empty(w.norm.rows, dtype=torch.float32, device=dev)
+            self.h = torch.empty_like(g)
+            self.codes = torch.empty(lmbp.codes_words(g.numel()), dtype=torch.int32, device=dev)
+            self.dg = torch.empty_like(dy)
+            self.dx = torch.empty_like(dz)
+
+        def kernels(self):
+            return [lambda: nfwd(self.x, eps, z=self.z, rstd=self.rstd, stream=stream),
+                    lambda: afwd(self.g, y=self.h, codes=self.codes, stream=stream),
+                    lambda: abwd(self.dy, self.codes, dx=self.dg, stream=stream),
+                    lambda: nbwd(self.dz, self.z, self.rstd, dx=self.dx, stream=stream)]
+
+    main = Set(x, dz, g, dy)
+    step_kernels = main.kernels()
+
+    def step():
+        for k in step_kernels:
+            k()
 
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup} steps done; timing {args.steps}", file=sys.stderr, flush=True)
 
+    # Timed region: K steps back to back, bracketed by events on the kernels' stream.
     mk = lambda: torch.cuda.Event(enable_timing=True)
-    evs = [[mk() for _ in range(5)] for _ in range(args.steps)]
     start, end = mk(), mk()
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     start.record(stream)
-    for k in range(args.steps):
-        step(evs[k])
+    for _ in range(args.steps):
+        step()
     end.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
-
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
-    per_kernel_ms = {n: float(np.mean([e[i].elapsed_time(e[i + 1]) for e in evs]))
-                     for i, n in enumerate(names)}
+
+    # Per-kernel launch duration: each kernel launched back to back, cycling over
+    # three tensor sets (the working set of consecutive launches differs, so no
+    # launch reads what the previous one left in the 256 MB memory-side cache), timed
+    # with events around the launches on the same stream.
+    print("[bench] per-kernel timing", file=sys.stderr, flush=True)
+    sets = [main] + [Set(x.clone(), dz.clone(), g.clone(), dy.clone()) for _ in range(2)]
+    for st in sets:
+        for k in st.kernels():
+            k()
+    torch.cuda.synchronize()
+    per_kernel_ms = {}
+    for i, n in enumerate(names):
+        ks = [st.kernels()[i] for st in sets]
+        for j in range(3):
+            ks[j % 3]()
+        a, b = mk(), mk()
+        a.record(stream)
+        for j in range(args.steps):
+            ks[j % 3]()
+        b.record(stream)
+        torch.cuda.synchronize()
+        per_kernel_ms[n] = a.elapsed_time(b) / args.steps
+    del sets
+
+    # Plain-copy reference of known size: the practical streaming ceiling, and the
+    # calibration point for hardware byte counters.
+    copy_bytes = 384 * 2 ** 20
+    pairs = [(torch.ones(copy_bytes, dtype=torch.uint8, device=dev),
+              torch.empty(copy_bytes, dtype=torch.uint8, device=dev)) for _ in range(3)]
+    for src, dst in pairs:
+        lmbp.copy_bytes(src, dst, stream=stream)
+    a, b = mk(), mk()
+    a.record(stream)
+    for j in range(args.steps):
+        src, dst = pairs[j % 3]
+        lmbp.copy_bytes(src, dst, stream=stream)
+    b.record(stream)
+    torch.cuda.synchronize()
+    copy_ms = a.elapsed_time(b) / args.steps
+    del pairs
+
     bytes_step = sum(nb.values())
     value = bytes_step / (ms_step * 1e-3) / 1e9
     per_kernel = {n: {"us": round(per_kernel_ms[n] * 1e3, 2),
@@ -237,6 +280,9 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": load_traffic(dominant),
         },
+        "copy_reference": {"bytes_moved": 2 * copy_bytes, "us": round(copy_ms * 1e3, 2),
+                           "GBps": round(2 * copy_bytes / (copy_ms * 1e-3) / 1e9, 1)},
+        "inter_kernel_us_per_step": round(ms_step * 1e3 - sum(per_kernel_ms.values()) * 1e3, 2),
         "wall_s_timed": round(t_wall, 4),
     }
     if not args.no_cpu_baseline:

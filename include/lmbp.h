@@ -118,7 +118,7 @@ lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void *dz,
 
 /* ------------------------------------------------------------------------
  * Measurement utility (not part of the method): copies `bytes` bytes from src
- * to dst with 16-byte vector loads and stores. src and dst must be 16-byte
+ * to dst with 16-byte non-temporal vector loads and stores. src and dst must be 16-byte
  * aligned and must not overlap. Used as the plain-copy reference for bandwidth
  * and hardware-counter calibration.
  * ------------------------------------------------------------------------ */

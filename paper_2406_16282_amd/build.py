@@ -44,25 +44,28 @@ def _run(cmd):
     return out
 
 
-def build(verbose=False):
+def build(verbose=False, defines=(), lib_path=LIB_PATH, build_dir=BUILD_DIR):
+    """Compile and link the library. `defines` are extra -D macros (tuning knobs
+    of the kernel sources); the defaults produce the shipped configuration."""
     hipcc = _hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
+    os.makedirs(build_dir, exist_ok=True)
+    flags = COMMON_FLAGS + [f"-D{d}" for d in defines]
     objs = []
     cmds = []
     for src in SOURCES:
-        obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
+        obj = os.path.join(build_dir, src.replace(".hip", ".o"))
         objs.append(obj)
-        cmds.append([hipcc, *COMMON_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj])
+        cmds.append([hipcc, *flags, "-c", os.path.join(CSRC, src), "-o", obj])
     with cf.ThreadPoolExecutor(max_workers=len(cmds)) as ex:
         logs = list(ex.map(_run, cmds))
-    tmp = LIB_PATH + ".tmp"
+    tmp = lib_path + ".tmp"
     logs.append(_run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]))
-    os.replace(tmp, LIB_PATH)
+    os.replace(tmp, lib_path)
     if verbose:
         for l in logs:
             if l.strip():
                 print(l)
-    return LIB_PATH
+    return lib_path
 
 
 if __name__ == "__main__":

@@ -19,7 +19,23 @@
 
 #include <type_traits>
 
+#ifndef LMBP_ACT_VPL
+// 16-byte vectors per lane in one wave tile (fp32 uses at least 4: one code word
+// spans 4 lanes). Small tiles mean many short-lived waves, which measured best.
+#define LMBP_ACT_VPL 2
+#endif
+#ifndef LMBP_ACT_NT
+// Non-temporal data loads (bit 0) / stores (bit 1) / code words (bit 2). Inputs and
+// outputs are touched once, so both stream; the 4-byte code-word accesses are
+// faster with the default policy.
+#define LMBP_ACT_NT 3
+#endif
+
 namespace lmbp {
+
+constexpr bool kActNtLoad = (LMBP_ACT_NT & 1) != 0;
+constexpr bool kActNtStore = (LMBP_ACT_NT & 2) != 0;
+constexpr bool kActNtCodes = (LMBP_ACT_NT & 4) != 0;
 
 // ------------------------------------------------------------------ constants
 // Appendix E: weights a* and biases c* of the three-ReLU combinations.
@@ -178,7 +194,7 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
     const int64_t vbase = base / E;
     u32x4 in[VPL];
 #pragma unroll
-    for (int j = 0; j < VPL; ++j) in[j] = ldg16(x, vbase + j * kWave + lane);
+    for (int j = 0; j < VPL; ++j) in[j] = ldg16<kActNtLoad>(x, vbase + j * kWave + lane);
 
     uint32_t part[VPL];
 #pragma unroll
@@ -192,7 +208,7 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
         p |= seg_code<A>(f[e]) << (2 * e);
       }
       part[j] = p;
-      stg16(y, vbase + j * kWave + lane, IO::pack(o));
+      stg16<kActNtStore>(y, vbase + j * kWave + lane, IO::pack(o));
     }
 
     const int q = lane % G;
@@ -218,7 +234,9 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
         const uint32_t mask = (PART == 32) ? 0xffffffffu : ((1u << PART) - 1u);
         word |= (recv & mask) << (((q + s) % G) * PART);
       }
-      codes[wbase + int64_t(G * m + q) * (kWave / G) + lane / G] = word;
+      uint32_t* cw = codes + wbase + int64_t(G * m + q) * (kWave / G) + lane / G;
+      if constexpr (kActNtCodes) __builtin_nontemporal_store(word, cw);
+      else *cw = word;
     }
     return;
   }
@@ -262,8 +280,10 @@ __global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
     uint32_t word[VPL];
 #pragma unroll
     for (int j = 0; j < VPL; ++j) {
-      in[j] = ldg16(dy, vbase + j * kWave + lane);
-      word[j] = codes[wbase + j * (kWave / G) + lane / G];
+      in[j] = ldg16<kActNtLoad>(dy, vbase + j * kWave + lane);
+      const uint32_t* cw = codes + wbase + j * (kWave / G) + lane / G;
+      if constexpr (kActNtCodes) word[j] = __builtin_nontemporal_load(cw);
+      else word[j] = *cw;
     }
 #pragma unroll
     for (int j = 0; j < VPL; ++j) {
@@ -272,7 +292,7 @@ __global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
       IO::unpack(in[j], f);
 #pragma unroll
       for (int e = 0; e < E; ++e) f[e] = f[e] * seg_slope<A>((p >> (2 * e)) & 3u);
-      stg16(dx, vbase + j * kWave + lane, IO::pack(f));
+      stg16<kActNtStore>(dx, vbase + j * kWave + lane, IO::pack(f));
     }
     return;
   }
@@ -286,9 +306,12 @@ __global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
 
 // ------------------------------------------------------------------ launchers
 namespace {
-constexpr int kActVPL = 4;
 template <class IO>
-constexpr int64_t act_tile() { return int64_t(kWave) * kActVPL * IO::kPerVec; }
+constexpr int act_vpl() {
+  return (IO::kPerVec == 4 && LMBP_ACT_VPL < 4) ? 4 : LMBP_ACT_VPL;
+}
+template <class IO>
+constexpr int64_t act_tile() { return int64_t(kWave) * act_vpl<IO>() * IO::kPerVec; }
 template <class IO>
 int64_t act_blocks(int64_t n) {
   const int64_t waves = (n + act_tile<IO>() - 1) / act_tile<IO>();
@@ -301,7 +324,7 @@ hipError_t launch_act_fwd_t(int64_t n, const void* x, void* y, uint32_t* codes, 
                             hipStream_t s) {
   const int64_t blocks = act_blocks<IO>(n);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((act_fwd_kernel<IO, ACT, kActVPL>), dim3(unsigned(blocks)), dim3(256), 0, s,
+  hipLaunchKernelGGL((act_fwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(256), 0, s,
                      x, y, codes, n, int(vec_ok));
   return hipGetLastError();
 }
@@ -311,7 +334,7 @@ hipError_t launch_act_bwd_t(int64_t n, const void* dy, const uint32_t* codes, vo
                             bool vec_ok, hipStream_t s) {
   const int64_t blocks = act_blocks<IO>(n);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((act_bwd_kernel<IO, ACT, kActVPL>), dim3(unsigned(blocks)), dim3(256), 0, s,
+  hipLaunchKernelGGL((act_bwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(256), 0, s,
                      dy, codes, dx, n, int(vec_ok));
   return hipGetLastError();
 }

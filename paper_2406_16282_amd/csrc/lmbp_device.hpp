@@ -67,12 +67,24 @@ struct BF16 {
   }
 };
 
+// 16-byte global loads / stores. NT selects the non-temporal (streaming) cache
+// policy, for data that is touched exactly once.
+template <bool NT = false>
 __device__ inline u32x4 ldg16(const void* base, int64_t vec_index) {
-  return reinterpret_cast<const u32x4*>(base)[vec_index];
+  const u32x4* p = reinterpret_cast<const u32x4*>(base) + vec_index;
+  if constexpr (NT) return __builtin_nontemporal_load(p);
+  else return *p;
 }
+template <bool NT = false>
 __device__ inline void stg16(void* base, int64_t vec_index, const u32x4& v) {
-  reinterpret_cast<u32x4*>(base)[vec_index] = v;
+  u32x4* p = reinterpret_cast<u32x4*>(base) + vec_index;
+  if constexpr (NT) __builtin_nontemporal_store(v, p);
+  else *p = v;
 }
+
+// Compiler-only barrier: makes `v` opaque so that values derived from it are
+// recomputed after this point instead of being kept live in registers.
+__device__ inline void opaque(u32x4& v) { asm volatile("" : "+v"(v)); }
 
 // Cross-lane move inside groups of 4 lanes (DPP quad_perm): lane q of every quad
 // receives `v` from lane perm[q] of the same quad.

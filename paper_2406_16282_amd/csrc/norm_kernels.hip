@@ -4,11 +4,12 @@
 // rstd = 1 / sigma, where H x = x - mean(x) (LN) or x (RMS). Backward from the saved
 // output alone: dx = rstd * (H dz - z * p^-1 z^T dz).
 //
-// Fast path: one wave per row, the row held in registers (VPL 16-byte vectors per
-// lane, lane l holding vectors l, l + 64, ...), so each tensor is read from HBM once
-// and every statistic is a register pass plus a wave reduction. Rows that are not
-// 16-byte aligned, or wider than the register tile, use a block-per-row path that
-// re-reads the row for each pass.
+// Fast path: 1, 2 or 4 waves per row (chosen from the row width), the row held in
+// registers (thread t of a row holding 16-byte vectors t, t + 64*WPR, ...), so each
+// tensor is read from HBM once and every statistic is a register pass plus a wave
+// reduction (and one LDS exchange when a row spans several waves). Rows that are
+// not 16-byte aligned, or wider than 4 waves x 16 vectors, use a block-per-row path
+// that re-reads the row for each pass.
 //
 // Numerics: LN accumulates x - x0 (x0 = the row's first element) so that rows
 // with a large common offset do not lose the deviations to rounding; the centred
@@ -19,100 +20,145 @@
 
 namespace lmbp {
 
-template <class IO>
-__device__ inline float first_elem(const u32x4& v) {
-  float f[IO::kPerVec];
-  IO::unpack(v, f);
-  return f[0];
+#ifndef LMBP_NORM_NT
+// Non-temporal loads (bit 0) / stores (bit 1). Streaming stores keep the outputs
+// out of the caches, so no dirty lines are left for the end-of-kernel write-back
+// or for the next kernel to evict; inputs are read with the default policy.
+#define LMBP_NORM_NT 2
+#endif
+constexpr bool kNormNtLoad = (LMBP_NORM_NT & 1) != 0;
+constexpr bool kNormNtStore = (LMBP_NORM_NT & 2) != 0;
+
+// Sum over the WPR waves that share a row (blockDim.x == 256, the row's waves
+// consecutive in the block). `slot` must be used by one call per kernel, so the
+// LDS words are written once and one barrier suffices. Every thread of the block
+// must call it.
+template <int WPR, int NS>
+__device__ inline void row_sums(float (&v)[NS], float (*red)[256 / kWave]) {
+#pragma unroll
+  for (int i = 0; i < NS; ++i) v[i] = wave_sum(v[i]);
+  if constexpr (WPR > 1) {
+    const int wave = threadIdx.x / kWave;
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+#pragma unroll
+      for (int i = 0; i < NS; ++i) red[i][wave] = v[i];
+    }
+    __syncthreads();
+    const int first = (wave / WPR) * WPR;
+#pragma unroll
+    for (int i = 0; i < NS; ++i) {
+      float t = 0.0f;
+#pragma unroll
+      for (int k = 0; k < WPR; ++k) t += red[i][first + k];
+      v[i] = t;
+    }
+  }
 }
 
-template <class IO, bool LN, int VPL>
+// Register-tile path: WPR waves per row, thread t of the row (0 <= t < 64*WPR)
+// holding vectors t, t + 64*WPR, ... (VPL of them). Rows start on 16-byte
+// boundaries (checked by the host).
+template <class IO, bool LN, int VPL, int WPR>
 __global__ __launch_bounds__(256) void norm_fwd_vec(const void* x, void* z, float* __restrict__ rstd,
                                                     int64_t rows, int cols, float eps) {
   constexpr int E = IO::kPerVec;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
-  if (row >= rows) return;
+  constexpr int TPR = kWave * WPR;
+  constexpr int RPB = 256 / TPR;
+  __shared__ float red[2][256 / kWave];
+  const int t = threadIdx.x % TPR;
+  const int64_t row = int64_t(blockIdx.x) * RPB + threadIdx.x / TPR;
+  const bool active = row < rows;
+  if constexpr (WPR == 1) {
+    if (!active) return;  // no barriers in the single-wave path
+  }
   const int nv = cols / E;
   const int64_t vbase = row * nv;
 
   u32x4 v[VPL];
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
-    const int idx = j * kWave + lane;
-    v[j] = (idx < nv) ? ldg16(x, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
+    const int idx = j * TPR + t;
+    v[j] = (active && idx < nv) ? ldg16<kNormNtLoad>(x, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
   }
 
   float pivot = 0.0f, mean_d = 0.0f;
   if constexpr (LN) {
-    pivot = __builtin_bit_cast(float, __builtin_amdgcn_readfirstlane(
-                                          __builtin_bit_cast(int, first_elem<IO>(v[0]))));
-    float s1 = 0.0f;
+    pivot = active ? IO::load1(x, row * int64_t(cols)) : 0.0f;
+    float s[1] = {0.0f};
 #pragma unroll
     for (int j = 0; j < VPL; ++j) {
-      if (j * kWave + lane < nv) {
+      if (j * TPR + t < nv) {
         float f[E];
         IO::unpack(v[j], f);
 #pragma unroll
-        for (int e = 0; e < E; ++e) s1 += f[e] - pivot;
+        for (int e = 0; e < E; ++e) s[0] += f[e] - pivot;
       }
     }
-    mean_d = wave_sum(s1) / float(cols);
+    row_sums<WPR>(s, &red[0]);
+    mean_d = s[0] / float(cols);
   }
 
-  float s2 = 0.0f;
+  float q[1] = {0.0f};
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
-    if (j * kWave + lane < nv) {
+    if (j * TPR + t < nv) {
       float f[E];
       IO::unpack(v[j], f);
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         const float c = LN ? (f[e] - pivot) - mean_d : f[e];
-        s2 = __builtin_fmaf(c, c, s2);
+        q[0] = __builtin_fmaf(c, c, q[0]);
       }
     }
   }
-  const float var = wave_sum(s2) / float(cols);
-  const float rs = rsqrtf(var + eps);
+  row_sums<WPR>(q, &red[1]);
+  const float rs = rsqrtf(q[0] / float(cols) + eps);
+  if (!active) return;
 
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
-    const int idx = j * kWave + lane;
+    opaque(v[j]);
+    const int idx = j * TPR + t;
     if (idx < nv) {
       float f[E];
       IO::unpack(v[j], f);
 #pragma unroll
       for (int e = 0; e < E; ++e) f[e] = (LN ? (f[e] - pivot) - mean_d : f[e]) * rs;
-      stg16(z, vbase + idx, IO::pack(f));
+      stg16<kNormNtStore>(z, vbase + idx, IO::pack(f));
     }
   }
-  if (lane == 0) rstd[row] = rs;
+  if (t == 0) rstd[row] = rs;
 }
 
-template <class IO, bool LN, int VPL>
+template <class IO, bool LN, int VPL, int WPR>
 __global__ __launch_bounds__(256) void norm_bwd_vec(const void* dz, const void* z,
                                                     const float* __restrict__ rstd, void* dx,
                                                     int64_t rows, int cols) {
   constexpr int E = IO::kPerVec;
-  const int lane = threadIdx.x & (kWave - 1);
-  const int64_t row = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
-  if (row >= rows) return;
+  constexpr int TPR = kWave * WPR;
+  constexpr int RPB = 256 / TPR;
+  __shared__ float red[2][256 / kWave];
+  const int t = threadIdx.x % TPR;
+  const int64_t row = int64_t(blockIdx.x) * RPB + threadIdx.x / TPR;
+  const bool active = row < rows;
+  if constexpr (WPR == 1) {
+    if (!active) return;
+  }
   const int nv = cols / E;
   const int64_t vbase = row * nv;
 
   u32x4 vg[VPL], vz[VPL];
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
-    const int idx = j * kWave + lane;
-    const bool ok = idx < nv;
-    vg[j] = ok ? ldg16(dz, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
-    vz[j] = ok ? ldg16(z, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
+    const int idx = j * TPR + t;
+    const bool ok = active && idx < nv;
+    vg[j] = ok ? ldg16<kNormNtLoad>(dz, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
+    vz[j] = ok ? ldg16<kNormNtLoad>(z, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
   }
-  const float rs = rstd[row];
+  const float rs = active ? rstd[row] : 0.0f;
 
   // Zero padding contributes nothing to either sum.
-  float s_g = 0.0f, s_zg = 0.0f;
+  float s[2] = {0.0f, 0.0f};
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
     float g[E], zz[E];
@@ -120,23 +166,27 @@ __global__ __launch_bounds__(256) void norm_bwd_vec(const void* dz, const void* 
     IO::unpack(vz[j], zz);
 #pragma unroll
     for (int e = 0; e < E; ++e) {
-      if constexpr (LN) s_g += g[e];
-      s_zg = __builtin_fmaf(zz[e], g[e], s_zg);
+      if constexpr (LN) s[0] += g[e];
+      s[1] = __builtin_fmaf(zz[e], g[e], s[1]);
     }
   }
-  const float a = LN ? wave_sum(s_g) / float(cols) : 0.0f;
-  const float b = wave_sum(s_zg) / float(cols);
+  row_sums<WPR>(s, red);
+  if (!active) return;
+  const float a = LN ? s[0] / float(cols) : 0.0f;
+  const float b = s[1] / float(cols);
 
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
-    const int idx = j * kWave + lane;
+    opaque(vg[j]);
+    opaque(vz[j]);
+    const int idx = j * TPR + t;
     if (idx < nv) {
       float g[E], zz[E];
       IO::unpack(vg[j], g);
       IO::unpack(vz[j], zz);
 #pragma unroll
       for (int e = 0; e < E; ++e) g[e] = rs * __builtin_fmaf(-zz[e], b, g[e] - a);
-      stg16(dx, vbase + idx, IO::pack(g));
+      stg16<kNormNtStore>(dx, vbase + idx, IO::pack(g));
     }
   }
 }
@@ -202,51 +252,66 @@ __global__ __launch_bounds__(256) void norm_bwd_any(const void* dz, const void* 
 
 // ------------------------------------------------------------------ launchers
 namespace {
-// Register tiles available to the fast path, in 16-byte vectors per lane.
-constexpr int kVplChoices[] = {1, 2, 3, 4, 6, 8, 12, 16};
-constexpr int kMaxVpl = 16;
-
-template <class IO, bool LN, int VPL>
-hipError_t fwd_vec(int64_t rows, int cols, float eps, const void* x, void* z, float* rstd,
-                   hipStream_t s) {
-  const int64_t blocks = (rows + 3) / 4;
-  hipLaunchKernelGGL((norm_fwd_vec<IO, LN, VPL>), dim3(unsigned(blocks)), dim3(256), 0, s, x, z, rstd,
-                     rows, cols, eps);
-  return hipGetLastError();
-}
-template <class IO, bool LN, int VPL>
-hipError_t bwd_vec(int64_t rows, int cols, const void* dz, const void* z, const float* rstd,
-                   void* dx, hipStream_t s) {
-  const int64_t blocks = (rows + 3) / 4;
-  hipLaunchKernelGGL((norm_bwd_vec<IO, LN, VPL>), dim3(unsigned(blocks)), dim3(256), 0, s, dz, z, rstd,
-                     dx, rows, cols);
-  return hipGetLastError();
-}
+// Launch shape of the register-tile path: WPR waves per row and VPL 16-byte
+// vectors per thread, chosen from the row width in vectors (nv). Narrow rows get
+// one wave (no barrier); wider rows spread over 2 or 4 waves so that each thread
+// holds at most 2 vectors while possible, which keeps registers low, occupancy
+// high and many rows in flight per CU. Rows beyond 4 waves x 16 vectors take
+// the block-per-row path.
+struct NormShape {
+  int wpr, vpl;
+};
+constexpr int kVplWide[] = {1, 2, 3, 4, 6, 8, 12, 16};
 
 template <class IO>
-int pick_vpl(int64_t cols) {
+NormShape pick_shape(int64_t cols) {
   const int64_t nv = cols / IO::kPerVec;
-  for (int v : kVplChoices)
-    if (int64_t(kWave) * v >= nv) return v;
-  return 0;
+  if (nv <= 64) return {1, 1};
+  if (nv <= 128) return {1, 2};
+  if (nv <= 256) return {2, 2};
+  for (int v : kVplWide)
+    if (int64_t(4) * kWave * v >= nv) return {4, v};
+  return {0, 0};
+}
+
+template <class IO, bool LN, int VPL, int WPR>
+hipError_t fwd_vec(int64_t rows, int cols, float eps, const void* x, void* z, float* rstd,
+                   hipStream_t s) {
+  constexpr int rpb = 4 / WPR;
+  const int64_t blocks = (rows + rpb - 1) / rpb;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((norm_fwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(256), 0, s, x, z,
+                     rstd, rows, cols, eps);
+  return hipGetLastError();
+}
+template <class IO, bool LN, int VPL, int WPR>
+hipError_t bwd_vec(int64_t rows, int cols, const void* dz, const void* z, const float* rstd,
+                   void* dx, hipStream_t s) {
+  constexpr int rpb = 4 / WPR;
+  const int64_t blocks = (rows + rpb - 1) / rpb;
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((norm_bwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(256), 0, s, dz, z,
+                     rstd, dx, rows, cols);
+  return hipGetLastError();
 }
 
 template <class IO, bool LN>
 hipError_t norm_fwd_t(int64_t rows, int64_t cols, float eps, const void* x, void* z, float* rstd,
                       bool vec_ok, hipStream_t s) {
-  const int vpl = vec_ok ? pick_vpl<IO>(cols) : 0;
-  if (vpl > 0 && (rows + 3) / 4 <= 0x7fffffff) {
-    const int c = int(cols);
-    switch (vpl) {
-      case 1: return fwd_vec<IO, LN, 1>(rows, c, eps, x, z, rstd, s);
-      case 2: return fwd_vec<IO, LN, 2>(rows, c, eps, x, z, rstd, s);
-      case 3: return fwd_vec<IO, LN, 3>(rows, c, eps, x, z, rstd, s);
-      case 4: return fwd_vec<IO, LN, 4>(rows, c, eps, x, z, rstd, s);
-      case 6: return fwd_vec<IO, LN, 6>(rows, c, eps, x, z, rstd, s);
-      case 8: return fwd_vec<IO, LN, 8>(rows, c, eps, x, z, rstd, s);
-      case 12: return fwd_vec<IO, LN, 12>(rows, c, eps, x, z, rstd, s);
-      default: return fwd_vec<IO, LN, kMaxVpl>(rows, c, eps, x, z, rstd, s);
-    }
+  const NormShape sh = vec_ok ? pick_shape<IO>(cols) : NormShape{0, 0};
+  const int c = int(cols);
+  switch (sh.wpr * 100 + sh.vpl) {
+    case 101: return fwd_vec<IO, LN, 1, 1>(rows, c, eps, x, z, rstd, s);
+    case 102: return fwd_vec<IO, LN, 2, 1>(rows, c, eps, x, z, rstd, s);
+    case 202: return fwd_vec<IO, LN, 2, 2>(rows, c, eps, x, z, rstd, s);
+    case 402: return fwd_vec<IO, LN, 2, 4>(rows, c, eps, x, z, rstd, s);
+    case 403: return fwd_vec<IO, LN, 3, 4>(rows, c, eps, x, z, rstd, s);
+    case 404: return fwd_vec<IO, LN, 4, 4>(rows, c, eps, x, z, rstd, s);
+    case 406: return fwd_vec<IO, LN, 6, 4>(rows, c, eps, x, z, rstd, s);
+    case 408: return fwd_vec<IO, LN, 8, 4>(rows, c, eps, x, z, rstd, s);
+    case 412: return fwd_vec<IO, LN, 12, 4>(rows, c, eps, x, z, rstd, s);
+    case 416: return fwd_vec<IO, LN, 16, 4>(rows, c, eps, x, z, rstd, s);
+    default: break;
   }
   if (rows > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((norm_fwd_any<IO, LN>), dim3(unsigned(rows)), dim3(256), 0, s, x, z, rstd, rows,
@@ -257,19 +322,20 @@ hipError_t norm_fwd_t(int64_t rows, int64_t cols, float eps, const void* x, void
 template <class IO, bool LN>
 hipError_t norm_bwd_t(int64_t rows, int64_t cols, const void* dz, const void* z, const float* rstd,
                       void* dx, bool vec_ok, hipStream_t s) {
-  const int vpl = vec_ok ? pick_vpl<IO>(cols) : 0;
-  if (vpl > 0 && (rows + 3) / 4 <= 0x7fffffff) {
-    const int c = int(cols);
-    switch (vpl) {
-      case 1: return bwd_vec<IO, LN, 1>(rows, c, dz, z, rstd, dx, s);
-      case 2: return bwd_vec<IO, LN, 2>(rows, c, dz, z, rstd, dx, s);
-      case 3: return bwd_vec<IO, LN, 3>(rows, c, dz, z, rstd, dx, s);
-      case 4: return bwd_vec<IO, LN, 4>(rows, c, dz, z, rstd, dx, s);
-      case 6: return bwd_vec<IO, LN, 6>(rows, c, dz, z, rstd, dx, s);
-      case 8: return bwd_vec<IO, LN, 8>(rows, c, dz, z, rstd, dx, s);
-      case 12: return bwd_vec<IO, LN, 12>(rows, c, dz, z, rstd, dx, s);
-      default: return bwd_vec<IO, LN, kMaxVpl>(rows, c, dz, z, rstd, dx, s);
-    }
+  const NormShape sh = vec_ok ? pick_shape<IO>(cols) : NormShape{0, 0};
+  const int c = int(cols);
+  switch (sh.wpr * 100 + sh.vpl) {
+    case 101: return bwd_vec<IO, LN, 1, 1>(rows, c, dz, z, rstd, dx, s);
+    case 102: return bwd_vec<IO, LN, 2, 1>(rows, c, dz, z, rstd, dx, s);
+    case 202: return bwd_vec<IO, LN, 2, 2>(rows, c, dz, z, rstd, dx, s);
+    case 402: return bwd_vec<IO, LN, 2, 4>(rows, c, dz, z, rstd, dx, s);
+    case 403: return bwd_vec<IO, LN, 3, 4>(rows, c, dz, z, rstd, dx, s);
+    case 404: return bwd_vec<IO, LN, 4, 4>(rows, c, dz, z, rstd, dx, s);
+    case 406: return bwd_vec<IO, LN, 6, 4>(rows, c, dz, z, rstd, dx, s);
+    case 408: return bwd_vec<IO, LN, 8, 4>(rows, c, dz, z, rstd, dx, s);
+    case 412: return bwd_vec<IO, LN, 12, 4>(rows, c, dz, z, rstd, dx, s);
+    case 416: return bwd_vec<IO, LN, 16, 4>(rows, c, dz, z, rstd, dx, s);
+    default: break;
   }
   if (rows > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((norm_bwd_any<IO, LN>), dim3(unsigned(rows)), dim3(256), 0, s, dz, z, rstd, dx,
@@ -296,6 +362,7 @@ hipError_t launch_norm_bwd(bool ln, bool bf16, int64_t rows, int64_t cols, const
 }
 
 // ---------------------------------------------------------- measurement copy
+// Plain streaming copy (the same non-temporal policy as the hot-path kernels).
 __global__ __launch_bounds__(256) void copy16_kernel(const u32x4* __restrict__ src,
                                                      u32x4* __restrict__ dst, int64_t nvec,
                                                      const uint8_t* __restrict__ src_tail,
@@ -306,12 +373,12 @@ __global__ __launch_bounds__(256) void copy16_kernel(const u32x4* __restrict__ s
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     const int64_t i = base + u * 256;
-    if (i < nvec) t[u] = src[i];
+    if (i < nvec) t[u] = ldg16<true>(src, i);
   }
 #pragma unroll
   for (int u = 0; u < kU; ++u) {
     const int64_t i = base + u * 256;
-    if (i < nvec) dst[i] = t[u];
+    if (i < nvec) stg16<true>(dst, i, t[u]);
   }
   if (blockIdx.x == 0 && threadIdx.x < tail) dst_tail[threadIdx.x] = src_tail[threadIdx.x];
 }

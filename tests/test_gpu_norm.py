@@ -56,9 +56,9 @@ CASES = [
     ("msln", "bf16", 2048, 768, 1.5, 1e-2, 1e-6),           # ViT-B bf16 rows (subset)
     ("msrms", "bf16", 512, 4096, 1.0, 1e-3, 1e-5),          # LLaMA-7B rows (subset)
     ("msrms", "fp32", 256, 4096, 1.0, 1e-3, 1e-5),
-    ("msln", "bf16", 64, 8192, 1.0, 1.0, 1e-6),             # widest register tile (bf16)
-    ("msrms", "fp32", 64, 4096 + 4, 1.0, 1.0, 1e-5),        # just past the fp32 tile: block path
-    ("msln", "bf16", 16, 8200, 1.0, 1.0, 1e-6),             # past the bf16 tile: block path
+    ("msln", "bf16", 5, 32768, 1.0, 1.0, 1e-6),             # widest register tile (bf16)
+    ("msrms", "fp32", 5, 16384 + 4, 1.0, 1.0, 1e-5),        # just past the fp32 tile: block path
+    ("msln", "bf16", 3, 32768 + 8, 1.0, 1.0, 1e-6),         # past the bf16 tile: block path
     ("msln", "fp32", 5, 1, 1.0, 1.0, 1e-6),                 # p = 1
     ("msrms", "bf16", 1, 8, 1.0, 1.0, 1e-5),                # one row, one vector
     ("msln", "fp32", 7, 72, 1.0, 1.0, 0.3),                 # large eps
@@ -71,6 +71,22 @@ def test_parity(op, dtype, rows, cols, xs, gs, eps):
     x = inputs.normal((rows, cols), xs, dtype, tensor_id=inputs.NORM_X)
     dz = inputs.normal((rows, cols), gs, dtype, tensor_id=inputs.NORM_DZ)
     check_norm(op, dtype, x, dz, eps, f"normal({rows}x{cols})")
+
+
+# One width per launch shape of the register-tile path: (waves per row, vectors per
+# thread) = (1,1), (1,2), (2,2), (4,2), (4,3), (4,4), (4,6), (4,8), (4,12), (4,16).
+SHAPE_WIDTHS = {"bf16": [512, 1024, 2048, 4096, 5120, 8192, 12288, 16384, 24576, 32768],
+                "fp32": [256, 512, 1024, 2048, 2560, 4096, 6144, 8192, 12288, 16384]}
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("op", ["msln", "msrms"])
+def test_every_launch_shape(op, dtype):
+    for k, cols in enumerate(SHAPE_WIDTHS[dtype]):
+        rows = 7  # not a multiple of the rows per block: the last block has idle rows
+        x = inputs.normal((rows, cols), 1.0, dtype, tensor_id=inputs.NORM_X, block=k)
+        dz = inputs.normal((rows, cols), 1.0, dtype, tensor_id=inputs.NORM_DZ, block=k)
+        check_norm(op, dtype, x, dz, 1e-5, f"shape({rows}x{cols})")
 
 
 @pytest.mark.parametrize("op", ["msrms", "msln"])
