@@ -1,7 +1,8 @@
 """Benchmark of the Approx-BP / MS-BP hot path on one MI355X.
 
 A step is one pass of the whole hot path over one batch of the LLaMA-7B-shaped
-workload (bf16 storage, fp32 arithmetic), in training order:
+workload (bf16 storage, fp32 arithmetic), in training order (the backward half
+consumes the state saved by the previous step's forward, so all inputs are cold):
 
     MS-RMSNorm forward   on x    [4*2048, 4096]   -> z, rstd
     ReSiLU2 forward      on gate [4*2048, 11008]  -> SiLU(gate), 2-bit codes
@@ -166,15 +167,26 @@ def main():
                     lambda: abwd(self.dy, self.codes, dx=self.dg, stream=stream),
                     lambda: nbwd(self.dz, self.z, self.rstd, dx=self.dx, stream=stream)]
 
-    main = Set(x, dz, g, dy)
-    step_kernels = main.kernels()
+    # Three tensor sets. Step k runs the forward kernels on set k % 3 and the backward
+    # kernels on set (k - 1) % 3, i.e. the backward consumes saved state written one
+    # full step (about 1.1 GB of traffic) earlier, as in training where a layer's
+    # forward and backward are separated by the rest of the network: no kernel finds
+    # its inputs in the 256 MB memory-side cache.
+    sets = [Set(x, dz, g, dy)] + [Set(x.clone(), dz.clone(), g.clone(), dy.clone()) for _ in range(2)]
+    ks = [st.kernels() for st in sets]
 
-    def step():
-        for k in step_kernels:
-            k()
+    def step(k):
+        f, b = ks[k % 3], ks[(k - 1) % 3]
+        f[0]()
+        f[1]()
+        b[2]()
+        b[3]()
 
-    for _ in range(args.warmup):
-        step()
+    for st in ks:          # every set holds valid saved state before the first step
+        st[0]()
+        st[1]()
+    for k in range(args.warmup):
+        step(k)
     torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup} steps done; timing {args.steps}", file=sys.stderr, flush=True)
 
@@ -184,37 +196,30 @@ def main():
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     start.record(stream)
-    for _ in range(args.steps):
-        step()
+    for k in range(args.steps):
+        step(args.warmup + k)
     end.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
 
-    # Per-kernel launch duration: each kernel launched back to back, cycling over
-    # three tensor sets (the working set of consecutive launches differs, so no
-    # launch reads what the previous one left in the 256 MB memory-side cache), timed
-    # with events around the launches on the same stream.
+    # Per-kernel launch duration: each kernel launched back to back, cycling over the
+    # three tensor sets (consecutive launches do not share a working set), timed with
+    # events around the launches on the same stream.
     print("[bench] per-kernel timing", file=sys.stderr, flush=True)
-    sets = [main] + [Set(x.clone(), dz.clone(), g.clone(), dy.clone()) for _ in range(2)]
-    for st in sets:
-        for k in st.kernels():
-            k()
-    torch.cuda.synchronize()
     per_kernel_ms = {}
     for i, n in enumerate(names):
-        ks = [st.kernels()[i] for st in sets]
         for j in range(3):
-            ks[j % 3]()
+            ks[j % 3][i]()
         a, b = mk(), mk()
         a.record(stream)
         for j in range(args.steps):
-            ks[j % 3]()
+            ks[j % 3][i]()
         b.record(stream)
         torch.cuda.synchronize()
         per_kernel_ms[n] = a.elapsed_time(b) / args.steps
-    del sets
+    del sets, ks
 
     # Plain-copy reference of known size: the practical streaming ceiling, and the
     # calibration point for hardware byte counters.

@@ -24,10 +24,13 @@
 // spans 4 lanes). Small tiles mean many short-lived waves, which measured best.
 #define LMBP_ACT_VPL 2
 #endif
+#ifndef LMBP_ACT_BLOCK
+#define LMBP_ACT_BLOCK 128  // threads per block (a multiple of 64)
+#endif
 #ifndef LMBP_ACT_NT
-// Non-temporal data loads (bit 0) / stores (bit 1) / code words (bit 2). Inputs and
-// outputs are touched once, so both stream; the 4-byte code-word accesses are
-// faster with the default policy.
+// Non-temporal data loads (bit 0) / data stores (bit 1) / code-word stores (bit 2) /
+// code-word loads (bit 3). Inputs and outputs are touched once, so both stream;
+// the 4-byte code-word accesses are faster with the default policy.
 #define LMBP_ACT_NT 3
 #endif
 
@@ -35,7 +38,8 @@ namespace lmbp {
 
 constexpr bool kActNtLoad = (LMBP_ACT_NT & 1) != 0;
 constexpr bool kActNtStore = (LMBP_ACT_NT & 2) != 0;
-constexpr bool kActNtCodes = (LMBP_ACT_NT & 4) != 0;
+constexpr bool kActNtCodeStore = (LMBP_ACT_NT & 4) != 0;
+constexpr bool kActNtCodeLoad = (LMBP_ACT_NT & 8) != 0;
 
 // ------------------------------------------------------------------ constants
 // Appendix E: weights a* and biases c* of the three-ReLU combinations.
@@ -174,7 +178,7 @@ using ActOf = typename std::conditional<ACT == kGelu, GeluAct, SiluAct>::type;
 
 // -------------------------------------------------------------------- kernels
 template <class IO, int ACT, int VPL>
-__global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
+__global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_fwd_kernel(const void* x, void* y,
                                                       uint32_t* __restrict__ codes,
                                                       int64_t n, int vec_ok) {
   using A = ActOf<ACT>;
@@ -183,7 +187,7 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
   constexpr int G = 16 / E;           // lanes sharing one code word
   constexpr int PART = 2 * E;         // code bits per vector
   constexpr int TILE = kWave * VPL * E;
-  static_assert(VPL % G == 0, "VPL must be a multiple of the lane group");
+  static_assert(VPL == 1 || VPL % G == 0, "VPL must be 1 or a multiple of the lane group");
 
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
@@ -213,6 +217,19 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
 
     const int q = lane % G;
     const int64_t wbase = base / 16;
+    if constexpr (VPL == 1) {
+      // One vector per lane: the G lanes of a group hold consecutive parts of one
+      // word. Each shifts its part into place and the group ORs them together (one
+      // or two DPP steps); the group's first lane stores the word.
+      uint32_t word = part[0] << (q * PART);
+      word |= group_rotate<G, 1>(word);
+      if constexpr (G == 4) word |= group_rotate<4, 2>(word);
+      if (q == 0) {
+        if constexpr (kActNtCodeStore) __builtin_nontemporal_store(word, codes + wbase + lane / G);
+        else codes[wbase + lane / G] = word;
+      }
+      return;
+    }
 #pragma unroll
     for (int m = 0; m < VPL / G; ++m) {
       uint32_t packed = 0;
@@ -235,7 +252,7 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
         word |= (recv & mask) << (((q + s) % G) * PART);
       }
       uint32_t* cw = codes + wbase + int64_t(G * m + q) * (kWave / G) + lane / G;
-      if constexpr (kActNtCodes) __builtin_nontemporal_store(word, cw);
+      if constexpr (kActNtCodeStore) __builtin_nontemporal_store(word, cw);
       else *cw = word;
     }
     return;
@@ -259,7 +276,7 @@ __global__ __launch_bounds__(256) void act_fwd_kernel(const void* x, void* y,
 }
 
 template <class IO, int ACT, int VPL>
-__global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
+__global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_bwd_kernel(const void* dy,
                                                       const uint32_t* __restrict__ codes,
                                                       void* dx, int64_t n, int vec_ok) {
   using A = ActOf<ACT>;
@@ -282,7 +299,7 @@ __global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
     for (int j = 0; j < VPL; ++j) {
       in[j] = ldg16<kActNtLoad>(dy, vbase + j * kWave + lane);
       const uint32_t* cw = codes + wbase + j * (kWave / G) + lane / G;
-      if constexpr (kActNtCodes) word[j] = __builtin_nontemporal_load(cw);
+      if constexpr (kActNtCodeLoad) word[j] = __builtin_nontemporal_load(cw);
       else word[j] = *cw;
     }
 #pragma unroll
@@ -308,14 +325,18 @@ __global__ __launch_bounds__(256) void act_bwd_kernel(const void* dy,
 namespace {
 template <class IO>
 constexpr int act_vpl() {
-  return (IO::kPerVec == 4 && LMBP_ACT_VPL < 4) ? 4 : LMBP_ACT_VPL;
+  // 1, or a multiple of the lanes sharing a code word (2 for bf16, 4 for fp32).
+  constexpr int g = 16 / IO::kPerVec;
+  return (LMBP_ACT_VPL == 1 || LMBP_ACT_VPL % g == 0) ? LMBP_ACT_VPL
+                                                      : ((LMBP_ACT_VPL + g - 1) / g) * g;
 }
 template <class IO>
 constexpr int64_t act_tile() { return int64_t(kWave) * act_vpl<IO>() * IO::kPerVec; }
 template <class IO>
 int64_t act_blocks(int64_t n) {
+  constexpr int wpb = LMBP_ACT_BLOCK / kWave;
   const int64_t waves = (n + act_tile<IO>() - 1) / act_tile<IO>();
-  return (waves + 3) / 4;
+  return (waves + wpb - 1) / wpb;
 }
 }  // namespace
 
@@ -324,7 +345,7 @@ hipError_t launch_act_fwd_t(int64_t n, const void* x, void* y, uint32_t* codes, 
                             hipStream_t s) {
   const int64_t blocks = act_blocks<IO>(n);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((act_fwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(256), 0, s,
+  hipLaunchKernelGGL((act_fwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(LMBP_ACT_BLOCK), 0, s,
                      x, y, codes, n, int(vec_ok));
   return hipGetLastError();
 }
@@ -334,7 +355,7 @@ hipError_t launch_act_bwd_t(int64_t n, const void* dy, const uint32_t* codes, vo
                             bool vec_ok, hipStream_t s) {
   const int64_t blocks = act_blocks<IO>(n);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((act_bwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(256), 0, s,
+  hipLaunchKernelGGL((act_bwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(LMBP_ACT_BLOCK), 0, s,
                      dy, codes, dx, n, int(vec_ok));
   return hipGetLastError();
 }

@@ -21,20 +21,33 @@
 namespace lmbp {
 
 #ifndef LMBP_NORM_NT
-// Non-temporal loads (bit 0) / stores (bit 1). Streaming stores keep the outputs
-// out of the caches, so no dirty lines are left for the end-of-kernel write-back
-// or for the next kernel to evict; inputs are read with the default policy.
-#define LMBP_NORM_NT 2
+// Non-temporal loads (bit 0) / stores (bit 1). Inputs and outputs are touched
+// once per launch, so both stream past the caches; measured on the whole step,
+// this beats default-policy loads even though a norm kernel alone reads faster
+// with them (the next kernels pay for the cached lines).
+#define LMBP_NORM_NT 3
 #endif
-constexpr bool kNormNtLoad = (LMBP_NORM_NT & 1) != 0;
-constexpr bool kNormNtStore = (LMBP_NORM_NT & 2) != 0;
+#ifndef LMBP_NORM_FWD_NT
+#define LMBP_NORM_FWD_NT LMBP_NORM_NT  // the forward kernel's policy
+#endif
+#ifndef LMBP_NORM_BWD_NT
+#define LMBP_NORM_BWD_NT LMBP_NORM_NT  // the backward kernel's policy
+#endif
+constexpr bool kFwdNtLoad = (LMBP_NORM_FWD_NT & 1) != 0;
+constexpr bool kFwdNtStore = (LMBP_NORM_FWD_NT & 2) != 0;
+constexpr bool kBwdNtLoad = (LMBP_NORM_BWD_NT & 1) != 0;
+constexpr bool kBwdNtStore = (LMBP_NORM_BWD_NT & 2) != 0;
 
-// Sum over the WPR waves that share a row (blockDim.x == 256, the row's waves
-// consecutive in the block). `slot` must be used by one call per kernel, so the
-// LDS words are written once and one barrier suffices. Every thread of the block
-// must call it.
+// Threads per block of the register-tile path: 256, or one row of WPR waves when
+// that is wider (WPR = 8).
+template <int WPR>
+constexpr int norm_block() { return WPR * kWave > 256 ? WPR * kWave : 256; }
+
+// Sum over the WPR waves that share a row (the row's waves consecutive in the
+// block). Each LDS slot is written by one call per kernel, so one barrier
+// suffices. Every thread of the block must call it.
 template <int WPR, int NS>
-__device__ inline void row_sums(float (&v)[NS], float (*red)[256 / kWave]) {
+__device__ inline void row_sums(float (&v)[NS], float (*red)[norm_block<WPR>() / kWave]) {
 #pragma unroll
   for (int i = 0; i < NS; ++i) v[i] = wave_sum(v[i]);
   if constexpr (WPR > 1) {
@@ -59,12 +72,13 @@ __device__ inline void row_sums(float (&v)[NS], float (*red)[256 / kWave]) {
 // holding vectors t, t + 64*WPR, ... (VPL of them). Rows start on 16-byte
 // boundaries (checked by the host).
 template <class IO, bool LN, int VPL, int WPR>
-__global__ __launch_bounds__(256) void norm_fwd_vec(const void* x, void* z, float* __restrict__ rstd,
-                                                    int64_t rows, int cols, float eps) {
+__global__ __launch_bounds__(norm_block<WPR>()) void norm_fwd_vec(const void* x, void* z,
+                                                                  float* __restrict__ rstd,
+                                                                  int64_t rows, int cols, float eps) {
   constexpr int E = IO::kPerVec;
   constexpr int TPR = kWave * WPR;
-  constexpr int RPB = 256 / TPR;
-  __shared__ float red[2][256 / kWave];
+  constexpr int RPB = norm_block<WPR>() / TPR;
+  __shared__ float red[2][norm_block<WPR>() / kWave];
   const int t = threadIdx.x % TPR;
   const int64_t row = int64_t(blockIdx.x) * RPB + threadIdx.x / TPR;
   const bool active = row < rows;
@@ -78,7 +92,7 @@ __global__ __launch_bounds__(256) void norm_fwd_vec(const void* x, void* z, floa
 #pragma unroll
   for (int j = 0; j < VPL; ++j) {
     const int idx = j * TPR + t;
-    v[j] = (active && idx < nv) ? ldg16<kNormNtLoad>(x, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
+    v[j] = (active && idx < nv) ? ldg16<kFwdNtLoad>(x, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
   }
 
   float pivot = 0.0f, mean_d = 0.0f;
@@ -124,20 +138,20 @@ __global__ __launch_bounds__(256) void norm_fwd_vec(const void* x, void* z, floa
       IO::unpack(v[j], f);
 #pragma unroll
       for (int e = 0; e < E; ++e) f[e] = (LN ? (f[e] - pivot) - mean_d : f[e]) * rs;
-      stg16<kNormNtStore>(z, vbase + idx, IO::pack(f));
+      stg16<kFwdNtStore>(z, vbase + idx, IO::pack(f));
     }
   }
   if (t == 0) rstd[row] = rs;
 }
 
 template <class IO, bool LN, int VPL, int WPR>
-__global__ __launch_bounds__(256) void norm_bwd_vec(const void* dz, const void* z,
-                                                    const float* __restrict__ rstd, void* dx,
-                                                    int64_t rows, int cols) {
+__global__ __launch_bounds__(norm_block<WPR>()) void norm_bwd_vec(const void* dz, const void* z,
+                                                                  const float* __restrict__ rstd,
+                                                                  void* dx, int64_t rows, int cols) {
   constexpr int E = IO::kPerVec;
   constexpr int TPR = kWave * WPR;
-  constexpr int RPB = 256 / TPR;
-  __shared__ float red[2][256 / kWave];
+  constexpr int RPB = norm_block<WPR>() / TPR;
+  __shared__ float red[2][norm_block<WPR>() / kWave];
   const int t = threadIdx.x % TPR;
   const int64_t row = int64_t(blockIdx.x) * RPB + threadIdx.x / TPR;
   const bool active = row < rows;
@@ -152,8 +166,8 @@ __global__ __launch_bounds__(256) void norm_bwd_vec(const void* dz, const void* 
   for (int j = 0; j < VPL; ++j) {
     const int idx = j * TPR + t;
     const bool ok = active && idx < nv;
-    vg[j] = ok ? ldg16<kNormNtLoad>(dz, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
-    vz[j] = ok ? ldg16<kNormNtLoad>(z, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
+    vg[j] = ok ? ldg16<kBwdNtLoad>(dz, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
+    vz[j] = ok ? ldg16<kBwdNtLoad>(z, vbase + idx) : u32x4{0u, 0u, 0u, 0u};
   }
   const float rs = active ? rstd[row] : 0.0f;
 
@@ -186,7 +200,7 @@ __global__ __launch_bounds__(256) void norm_bwd_vec(const void* dz, const void* 
       IO::unpack(vz[j], zz);
 #pragma unroll
       for (int e = 0; e < E; ++e) g[e] = rs * __builtin_fmaf(-zz[e], b, g[e] - a);
-      stg16<kNormNtStore>(dx, vbase + idx, IO::pack(g));
+      stg16<kBwdNtStore>(dx, vbase + idx, IO::pack(g));
     }
   }
 }
@@ -251,47 +265,60 @@ __global__ __launch_bounds__(256) void norm_bwd_any(const void* dz, const void* 
 }
 
 // ------------------------------------------------------------------ launchers
+#ifndef LMBP_NORM_TARGET_VPL
+#define LMBP_NORM_TARGET_VPL 2  // preferred upper bound on vectors per thread
+#endif
+#ifndef LMBP_NORM_MAX_WPR
+#define LMBP_NORM_MAX_WPR 4  // widest row group (waves per row)
+#endif
+
 namespace {
 // Launch shape of the register-tile path: WPR waves per row and VPL 16-byte
-// vectors per thread, chosen from the row width in vectors (nv). Narrow rows get
-// one wave (no barrier); wider rows spread over 2 or 4 waves so that each thread
-// holds at most 2 vectors while possible, which keeps registers low, occupancy
-// high and many rows in flight per CU. Rows beyond 4 waves x 16 vectors take
-// the block-per-row path.
+// vectors per thread, chosen from the row width in vectors (nv): the fewest waves
+// per row that keep VPL within the target (so registers stay low, occupancy high
+// and many rows are in flight per CU); rows wider than that use the widest group
+// with more vectors per thread, up to its capacity. Wider rows take the
+// block-per-row path.
 struct NormShape {
   int wpr, vpl;
 };
+constexpr int kVplSmall[] = {1, 2};
 constexpr int kVplWide[] = {1, 2, 3, 4, 6, 8, 12, 16};
 
 template <class IO>
 NormShape pick_shape(int64_t cols) {
   const int64_t nv = cols / IO::kPerVec;
-  if (nv <= 64) return {1, 1};
-  if (nv <= 128) return {1, 2};
-  if (nv <= 256) return {2, 2};
-  for (int v : kVplWide)
-    if (int64_t(4) * kWave * v >= nv) return {4, v};
+  for (int wpr = 1; wpr <= LMBP_NORM_MAX_WPR; wpr *= 2) {
+    if (int64_t(kWave) * wpr * LMBP_NORM_TARGET_VPL < nv) continue;
+    for (int v : kVplSmall)
+      if (int64_t(kWave) * wpr * v >= nv) return {wpr, v};
+  }
+  const int wpr = LMBP_NORM_MAX_WPR;
+  for (int v : kVplWide) {
+    if (wpr == 8 && v > 8) break;
+    if (int64_t(kWave) * wpr * v >= nv) return {wpr, v};
+  }
   return {0, 0};
 }
 
 template <class IO, bool LN, int VPL, int WPR>
 hipError_t fwd_vec(int64_t rows, int cols, float eps, const void* x, void* z, float* rstd,
                    hipStream_t s) {
-  constexpr int rpb = 4 / WPR;
+  constexpr int rpb = norm_block<WPR>() / (kWave * WPR);
   const int64_t blocks = (rows + rpb - 1) / rpb;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((norm_fwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(256), 0, s, x, z,
-                     rstd, rows, cols, eps);
+  hipLaunchKernelGGL((norm_fwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(norm_block<WPR>()),
+                     0, s, x, z, rstd, rows, cols, eps);
   return hipGetLastError();
 }
 template <class IO, bool LN, int VPL, int WPR>
 hipError_t bwd_vec(int64_t rows, int cols, const void* dz, const void* z, const float* rstd,
                    void* dx, hipStream_t s) {
-  constexpr int rpb = 4 / WPR;
+  constexpr int rpb = norm_block<WPR>() / (kWave * WPR);
   const int64_t blocks = (rows + rpb - 1) / rpb;
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((norm_bwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(256), 0, s, dz, z,
-                     rstd, dx, rows, cols);
+  hipLaunchKernelGGL((norm_bwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(norm_block<WPR>()),
+                     0, s, dz, z, rstd, dx, rows, cols);
   return hipGetLastError();
 }
 
@@ -303,7 +330,9 @@ hipError_t norm_fwd_t(int64_t rows, int64_t cols, float eps, const void* x, void
   switch (sh.wpr * 100 + sh.vpl) {
     case 101: return fwd_vec<IO, LN, 1, 1>(rows, c, eps, x, z, rstd, s);
     case 102: return fwd_vec<IO, LN, 2, 1>(rows, c, eps, x, z, rstd, s);
+    case 201: return fwd_vec<IO, LN, 1, 2>(rows, c, eps, x, z, rstd, s);
     case 202: return fwd_vec<IO, LN, 2, 2>(rows, c, eps, x, z, rstd, s);
+    case 401: return fwd_vec<IO, LN, 1, 4>(rows, c, eps, x, z, rstd, s);
     case 402: return fwd_vec<IO, LN, 2, 4>(rows, c, eps, x, z, rstd, s);
     case 403: return fwd_vec<IO, LN, 3, 4>(rows, c, eps, x, z, rstd, s);
     case 404: return fwd_vec<IO, LN, 4, 4>(rows, c, eps, x, z, rstd, s);
@@ -311,6 +340,12 @@ hipError_t norm_fwd_t(int64_t rows, int64_t cols, float eps, const void* x, void
     case 408: return fwd_vec<IO, LN, 8, 4>(rows, c, eps, x, z, rstd, s);
     case 412: return fwd_vec<IO, LN, 12, 4>(rows, c, eps, x, z, rstd, s);
     case 416: return fwd_vec<IO, LN, 16, 4>(rows, c, eps, x, z, rstd, s);
+    case 801: return fwd_vec<IO, LN, 1, 8>(rows, c, eps, x, z, rstd, s);
+    case 802: return fwd_vec<IO, LN, 2, 8>(rows, c, eps, x, z, rstd, s);
+    case 803: return fwd_vec<IO, LN, 3, 8>(rows, c, eps, x, z, rstd, s);
+    case 804: return fwd_vec<IO, LN, 4, 8>(rows, c, eps, x, z, rstd, s);
+    case 806: return fwd_vec<IO, LN, 6, 8>(rows, c, eps, x, z, rstd, s);
+    case 808: return fwd_vec<IO, LN, 8, 8>(rows, c, eps, x, z, rstd, s);
     default: break;
   }
   if (rows > 0x7fffffff) return hipErrorInvalidValue;
@@ -327,7 +362,9 @@ hipError_t norm_bwd_t(int64_t rows, int64_t cols, const void* dz, const void* z,
   switch (sh.wpr * 100 + sh.vpl) {
     case 101: return bwd_vec<IO, LN, 1, 1>(rows, c, dz, z, rstd, dx, s);
     case 102: return bwd_vec<IO, LN, 2, 1>(rows, c, dz, z, rstd, dx, s);
+    case 201: return bwd_vec<IO, LN, 1, 2>(rows, c, dz, z, rstd, dx, s);
     case 202: return bwd_vec<IO, LN, 2, 2>(rows, c, dz, z, rstd, dx, s);
+    case 401: return bwd_vec<IO, LN, 1, 4>(rows, c, dz, z, rstd, dx, s);
     case 402: return bwd_vec<IO, LN, 2, 4>(rows, c, dz, z, rstd, dx, s);
     case 403: return bwd_vec<IO, LN, 3, 4>(rows, c, dz, z, rstd, dx, s);
     case 404: return bwd_vec<IO, LN, 4, 4>(rows, c, dz, z, rstd, dx, s);
@@ -335,6 +372,12 @@ hipError_t norm_bwd_t(int64_t rows, int64_t cols, const void* dz, const void* z,
     case 408: return bwd_vec<IO, LN, 8, 4>(rows, c, dz, z, rstd, dx, s);
     case 412: return bwd_vec<IO, LN, 12, 4>(rows, c, dz, z, rstd, dx, s);
     case 416: return bwd_vec<IO, LN, 16, 4>(rows, c, dz, z, rstd, dx, s);
+    case 801: return bwd_vec<IO, LN, 1, 8>(rows, c, dz, z, rstd, dx, s);
+    case 802: return bwd_vec<IO, LN, 2, 8>(rows, c, dz, z, rstd, dx, s);
+    case 803: return bwd_vec<IO, LN, 3, 8>(rows, c, dz, z, rstd, dx, s);
+    case 804: return bwd_vec<IO, LN, 4, 8>(rows, c, dz, z, rstd, dx, s);
+    case 806: return bwd_vec<IO, LN, 6, 8>(rows, c, dz, z, rstd, dx, s);
+    case 808: return bwd_vec<IO, LN, 8, 8>(rows, c, dz, z, rstd, dx, s);
     default: break;
   }
   if (rows > 0x7fffffff) return hipErrorInvalidValue;
