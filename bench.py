@@ -41,7 +41,7 @@ KERNEL_SOURCES = ("paper_2406_16282_amd/csrc/act_kernels.hip",
                   "paper_2406_16282_amd/csrc/gelu_poly.h")
 
 
-def algorithmic_bytes(w):
+def algorithmic_bytes(w, swiglu=False):
     """Bytes each kernel must move once (reads + writes), per launch."""
     eb = 2 if w.norm.dtype == "bf16" else 4
     rows, p = w.norm.rows, w.norm.cols
@@ -49,11 +49,17 @@ def algorithmic_bytes(w):
     n_act = w.act.rows * w.act.cols
     ab = 2 if w.act.dtype == "bf16" else 4
     codes = 4 * ((n_act + 15) // 16)
+    if swiglu:
+        act = [("reswiglu2_fwd", 4 * n_act * ab + codes),          # g, u in; h, s out; codes out
+               ("reswiglu2_bwd", 5 * n_act * ab + codes)]          # dh, u, s, codes in; dg, du out
+    else:
+        act = [(f"{w.act.op}_fwd", 2 * n_act * ab + codes),        # x in, y out, codes out
+               (f"{w.act.op}_bwd", 2 * n_act * ab + codes)]        # dy, codes in, dx out
     return {
         f"{w.norm.op}_fwd": 2 * n_norm * eb + 4 * rows,            # x in, z out, rstd out
-        f"{w.act.op}_fwd": 2 * n_act * ab + codes,                 # x in, y out, codes out
-        f"{w.act.op}_bwd": 2 * n_act * ab + codes,                 # dy in, codes in, dx out
-        f"{w.norm.op}_bwd": 3 * n_norm * eb + 4 * rows,            # dz, z in, rstd in, dx out
+        act[0][0]: act[0][1],
+        act[1][0]: act[1][1],
+        f"{w.norm.op}_bwd": 3 * n_norm * eb + 4 * rows,            # dz, z, rstd in, dx out
     }
 
 
@@ -121,6 +127,8 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--swiglu", action="store_true",
+                    help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the hot path is row- and element-local and runs "
@@ -138,11 +146,12 @@ def main():
         sys.exit("bench.py needs a GPU")
     dev = torch.device("cuda:0")
     w = inputs.WORKLOADS[WORKLOAD]
-    nb = algorithmic_bytes(w)
+    nb = algorithmic_bytes(w, args.swiglu)
     eps = float(np.float32(w.norm.eps))
     print(f"[bench] generating {WORKLOAD} inputs", file=sys.stderr, flush=True)
     T = lambda a: inputs.storage_to_torch(a, dev)
     x, dz, g, dy = T(w.norm_x()), T(w.norm_dz()), T(w.act_x()), T(w.act_dy())
+    u = T(w.act_u()) if args.swiglu else None
     nfwd = {"msrms": lmbp.msrms_fwd, "msln": lmbp.msln_fwd}[w.norm.op]
     nbwd = {"msrms": lmbp.msrms_bwd, "msln": lmbp.msln_bwd}[w.norm.op]
     afwd = {"resilu2": lmbp.resilu2_fwd, "regelu2": lmbp.regelu2_fwd}[w.act.op]
@@ -152,19 +161,28 @@ def main():
 
     class Set:
         """One full set of step tensors (inputs and saved state / outputs)."""
-        def __init__(self, x, dz, g, dy):
-            self.x, self.dz, self.g, self.dy = x, dz, g, dy
+        def __init__(self, x, dz, g, dy, u):
+            self.x, self.dz, self.g, self.dy, self.u = x, dz, g, dy, u
             self.z = torch.empty_like(x)
             self.rstd = torch.empty(w.norm.rows, dtype=torch.float32, device=dev)
             self.h = torch.empty_like(g)
             self.codes = torch.empty(lmbp.codes_words(g.numel()), dtype=torch.int32, device=dev)
             self.dg = torch.empty_like(dy)
             self.dx = torch.empty_like(dz)
+            if u is not None:
+                self.s = torch.empty_like(g)
+                self.du = torch.empty_like(u)
 
         def kernels(self):
-            return [lambda: nfwd(self.x, eps, z=self.z, rstd=self.rstd, stream=stream),
-                    lambda: afwd(self.g, y=self.h, codes=self.codes, stream=stream),
-                    lambda: abwd(self.dy, self.codes, dx=self.dg, stream=stream),
+            if self.u is None:
+                act = [lambda: afwd(self.g, y=self.h, codes=self.codes, stream=stream),
+                       lambda: abwd(self.dy, self.codes, dx=self.dg, stream=stream)]
+            else:
+                act = [lambda: lmbp.reswiglu2_fwd(self.g, self.u, h=self.h, s=self.s, codes=self.codes,
+                                                  stream=stream),
+                       lambda: lmbp.reswiglu2_bwd(self.dy, self.u, self.s, self.codes, dg=self.dg,
+                                                  du=self.du, stream=stream)]
+            return [lambda: nfwd(self.x, eps, z=self.z, rstd=self.rstd, stream=stream), act[0], act[1],
                     lambda: nbwd(self.dz, self.z, self.rstd, dx=self.dx, stream=stream)]
 
     # Three tensor sets. Step k runs the forward kernels on set k % 3 and the backward
@@ -172,7 +190,9 @@ def main():
     # full step (about 1.1 GB of traffic) earlier, as in training where a layer's
     # forward and backward are separated by the rest of the network: no kernel finds
     # its inputs in the 256 MB memory-side cache.
-    sets = [Set(x, dz, g, dy)] + [Set(x.clone(), dz.clone(), g.clone(), dy.clone()) for _ in range(2)]
+    clone = lambda t: None if t is None else t.clone()
+    sets = [Set(x, dz, g, dy, u)] + [Set(x.clone(), dz.clone(), g.clone(), dy.clone(), clone(u))
+                                     for _ in range(2)]
     ks = [st.kernels() for st in sets]
 
     def step(k):
@@ -261,10 +281,11 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": WORKLOAD,
+            "workload": WORKLOAD + ("_fused" if args.swiglu else ""),
             "storage": w.act.dtype,
             "norm": f"{w.norm.op} [{w.norm.rows}x{w.norm.cols}] eps={w.norm.eps:g}",
-            "act": f"{w.act.op} [{w.act.rows}x{w.act.cols}]",
+            "act": (f"reswiglu2 (SiLU(g) * u) [{w.act.rows}x{w.act.cols}]" if args.swiglu
+                    else f"{w.act.op} [{w.act.rows}x{w.act.cols}]"),
             "bytes_per_step": bytes_step,
             "elements_per_step": 2 * (n_act + w.norm.rows * w.norm.cols),
         },
@@ -283,14 +304,14 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": load_traffic(dominant),
+            "traffic": load_traffic(dominant + ("_fused" if args.swiglu else "")),
         },
         "copy_reference": {"bytes_moved": 2 * copy_bytes, "us": round(copy_ms * 1e3, 2),
                            "GBps": round(2 * copy_bytes / (copy_ms * 1e-3) / 1e9, 1)},
         "inter_kernel_us_per_step": round(ms_step * 1e3 - sum(per_kernel_ms.values()) * 1e3, 2),
         "wall_s_timed": round(t_wall, 4),
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not args.swiglu:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(out))

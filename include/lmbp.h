@@ -8,6 +8,7 @@
  *   resilu2_fwd / resilu2_bwd   ReSiLU2  (Sec. 4.2; constants Appendix E)
  *   msln_fwd    / msln_bwd      MS-LN    (Sec. 5.2 Alg. 1; Appendix G Alg. 2)
  *   msrms_fwd   / msrms_bwd     MS-RMSNorm (Appendix G Alg. 3)
+ *   reswiglu2_fwd / reswiglu2_bwd  ReSiLU2 fused with the SwiGLU product (LLaMA MLP)
  *
  * Conventions shared by every call
  * --------------------------------
@@ -90,6 +91,29 @@ lmbp_status resilu2_fwd(lmbp_dtype dt, int64_t n, const void *x, void *y,
                         uint32_t *codes, void *stream);
 lmbp_status resilu2_bwd(lmbp_dtype dt, int64_t n, const void *dy,
                         const uint32_t *codes, void *dx, void *stream);
+
+/* ------------------------------------------------------------------------
+ * ReSiLU2 inside a SwiGLU product, h = SiLU(g) * u: the LLaMA MLP, where the paper
+ * substitutes ReSiLU2 for SiLU (Sec. 6). The backward is the Approx-BP backward of
+ * the product (Sec. 4.1): the exact product rule on the saved forward activation
+ * s = SiLU(g), and the step derivative of the three-ReLU combination for SiLU.
+ *
+ * Forward:  s = SiLU(g), h = s * u, codes of g (as resilu2_fwd).
+ * Backward: dg = dh * u * s[code],  du = dh * s.
+ *
+ *   g, u   : n elements of dtype (inputs). h: n elements (output; h == g or h == u
+ *            allowed). s: n elements (output, saved for the backward; overlaps
+ *            nothing). codes: lmbp_codes_bytes(n) bytes (output; overlaps nothing).
+ *   dh, u, s, codes (bwd): inputs; dg, du: n elements (outputs; dg == dh and
+ *            du == u allowed, no other overlap).
+ * Saved state per element: the 2-bit code plus s (which the product keeps anyway);
+ * g itself is not needed.
+ * ------------------------------------------------------------------------ */
+lmbp_status reswiglu2_fwd(lmbp_dtype dt, int64_t n, const void *g, const void *u,
+                          void *h, void *s, uint32_t *codes, void *stream);
+lmbp_status reswiglu2_bwd(lmbp_dtype dt, int64_t n, const void *dh, const void *u,
+                          const void *s, const uint32_t *codes, void *dg, void *du,
+                          void *stream);
 
 /* ------------------------------------------------------------------------
  * MS-LN (Sec. 5.2 Alg. 1, Appendix G Alg. 2) and MS-RMSNorm (Alg. 3), for a

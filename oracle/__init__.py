@@ -11,6 +11,8 @@ What it computes, each function citing the passage it follows:
   constants from Appendix E): exact GELU/SiLU forward, the 2-bit segment code of
   every element, LSB-first packing 16 codes per 32-bit word, and the backward pass
   ``dx = dy * (slope of the ReLU combination on the element's segment)``.
+* ``activations`` also holds ReSiLU2 inside a SwiGLU product (h = SiLU(g) * u), the
+  form it takes in the LLaMA MLP.
 * ``norms``: MS-LN and MS-RMSNorm (Sec. 5.2 Alg. 1; Appendix G Alg. 2 and Alg. 3):
   forward ``z = H x / sigma`` saving ``z`` and ``1/sigma``; backward
   ``dx = sigma^-1 (H - p^-1 z z^T) dz`` from the saved output alone.
@@ -28,6 +30,7 @@ from .activations import (
     relu_combination, derivative_levels, segment_code,
     gelu, silu, pack_codes, unpack_codes, codes_words,
     regelu2_fwd, regelu2_bwd, resilu2_fwd, resilu2_bwd,
+    reswiglu2_fwd, reswiglu2_bwd,
 )
 from .norms import msln_fwd, msln_bwd, msrms_fwd, msrms_bwd
 
@@ -37,5 +40,6 @@ __all__ = [
     "relu_combination", "derivative_levels", "segment_code",
     "gelu", "silu", "pack_codes", "unpack_codes", "codes_words",
     "regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd",
+    "reswiglu2_fwd", "reswiglu2_bwd",
     "msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd",
 ]

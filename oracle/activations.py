@@ -139,3 +139,32 @@ def resilu2_fwd(x):
 def resilu2_bwd(dy, words):
     """ReSiLU2 backward: dy times the step derivative of h~ for the SiLU constants."""
     return _act_bwd(dy, words, SILU_A)
+
+
+# ---------------------------------------------------------------- SwiGLU
+
+def reswiglu2_fwd(g, u):
+    """ReSiLU2 inside a SwiGLU product (the LLaMA MLP, where the paper substitutes
+    ReSiLU2 for SiLU, Sec. 6): s = SiLU(g), h = s * u, plus the 2-bit codes of g.
+
+    Returns (h, s, packed codes). s is what the product's backward needs; SiLU's own
+    backward needs only the codes (Sec. 4.2).
+    """
+    g = np.asarray(g, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    if g.shape != u.shape:
+        raise ValueError("g and u must have the same shape")
+    s = silu(g)
+    return s * u, s, pack_codes(segment_code(g, SILU_C))
+
+
+def reswiglu2_bwd(dh, u, s, words):
+    """Approximate backward of h = SiLU(g) * u (Sec. 4.1: the backward of the network
+    with h~ in place of SiLU, evaluated on the exact forward activations):
+    du = dh * s (the exact product rule, s = SiLU(g) from the forward),
+    dg = dh * u * slope of h~ at g (from the codes)."""
+    dh = np.asarray(dh, dtype=np.float64)
+    u = np.asarray(u, dtype=np.float64)
+    s = np.asarray(s, dtype=np.float64)
+    codes = unpack_codes(words, dh.size).reshape(dh.shape)
+    return dh * u * derivative_levels(SILU_A)[codes], dh * s

@@ -3,7 +3,7 @@ Memory-Sharing Backpropagation (Yang et al., ICML 2024).
 
 ReGELU2 / ReSiLU2 keep the exact activation in the forward pass and save only a
 2-bit segment code per element for a step-function derivative in the backward
-pass (Sec. 4.2). MS-LN / MS-RMSNorm, with the affine merged into the next linear
+pass (Sec. 4.2); ReSiLU2 also comes fused with the SwiGLU product of the LLaMA MLP. MS-LN / MS-RMSNorm, with the affine merged into the next linear
 layer, save only their output and one fp32 statistic per row (Sec. 5.2).
 
 The kernels live in liblmbp.so (C ABI in include/lmbp.h); ``binding`` marshals
@@ -24,4 +24,6 @@ from .binding import (  # noqa: F401
     regelu2_fwd,
     resilu2_bwd,
     resilu2_fwd,
+    reswiglu2_bwd,
+    reswiglu2_fwd,
 )

@@ -20,6 +20,7 @@ OK, EINVAL, EDTYPE, EOVERLAP, EHIP = 0, 1, 2, 3, 4
 
 ACT_OPS = ("regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd")
 NORM_OPS = ("msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd")
+GLU_OPS = ("reswiglu2_fwd", "reswiglu2_bwd")
 
 
 class LmbpError(RuntimeError):
@@ -60,6 +61,10 @@ def lib():
         fn = getattr(L, name)
         fn.argtypes = [i32, i64, i64, vp, vp, vp, vp, vp]
         fn.restype = i32
+    L.reswiglu2_fwd.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp]
+    L.reswiglu2_fwd.restype = i32
+    L.reswiglu2_bwd.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp]
+    L.reswiglu2_bwd.restype = i32
     L.lmbp_copy.argtypes = [vp, vp, i64, vp]
     L.lmbp_copy.restype = i32
     _lib = L
@@ -173,6 +178,42 @@ def resilu2_fwd(x, y=None, codes=None, stream=None):
 def resilu2_bwd(dy, codes, dx=None, stream=None):
     """ReSiLU2 backward: dx = dy * step derivative selected by the codes."""
     return _act_bwd("resilu2_bwd", dy, codes, dx, stream)
+
+
+def _same(t, ref, what):
+    _dev(t, what)
+    if t.dtype != ref.dtype or t.numel() != ref.numel() or t.device != ref.device:
+        raise ValueError(f"{what} must match {ref.dtype} x {ref.numel()} on {ref.device}")
+    return t
+
+
+def reswiglu2_fwd(g, u, h=None, s=None, codes=None, stream=None):
+    """ReSiLU2 in a SwiGLU product: returns (h = SiLU(g) * u, s = SiLU(g), codes of g)."""
+    _dev(g, "g")
+    dt = _dtype_code(g)
+    _same(u, g, "u")
+    h = _like(g, h, "h")
+    s = _like(g, s, "s")
+    codes = _codes_out(g.numel(), g.device, codes)
+    _check("reswiglu2_fwd", lib().reswiglu2_fwd(dt, g.numel(), _ptr(g), _ptr(u), _ptr(h), _ptr(s),
+                                                _ptr(codes), _stream(g, stream)))
+    return h, s, codes
+
+
+def reswiglu2_bwd(dh, u, s, codes, dg=None, du=None, stream=None):
+    """Backward of reswiglu2_fwd: returns (dg = dh * u * slope[code], du = dh * s)."""
+    _dev(dh, "dh")
+    dt = _dtype_code(dh)
+    _same(u, dh, "u")
+    _same(s, dh, "s")
+    _dev(codes, "codes")
+    if codes.dtype != torch.int32 or codes.numel() < codes_words(dh.numel()):
+        raise ValueError("codes must be the int32 buffer written by the forward")
+    dg = _like(dh, dg, "dg")
+    du = _like(dh, du, "du")
+    _check("reswiglu2_bwd", lib().reswiglu2_bwd(dt, dh.numel(), _ptr(dh), _ptr(u), _ptr(s), _ptr(codes),
+                                                _ptr(dg), _ptr(du), _stream(dh, stream)))
+    return dg, du
 
 
 def _rows_cols(t):

@@ -176,6 +176,75 @@ __device__ inline float act_value(float x) {
 template <int ACT>
 using ActOf = typename std::conditional<ACT == kGelu, GeluAct, SiluAct>::type;
 
+// Store the code words of one wave tile. part[j] holds the 2E code bits of this
+// lane's vector j (vector index tile_vec + j*64 + lane), G lanes sharing a word.
+//   VPL == 1: the G lanes of a group shift their parts into place and OR them
+//   together with one or two DPP steps; the group's first lane stores the word.
+//   VPL a multiple of G: each lane packs its parts of G consecutive vectors into one
+//   32-bit value and the group transposes them with DPP quad permutes (step s: lane q
+//   sends part (q - s) mod G and receives, from lane (q + s) mod G, that lane's part
+//   for vector G*m + q), so every lane stores a whole word and the stores of a wave
+//   are contiguous.
+template <class IO, int VPL>
+__device__ inline void store_tile_codes(uint32_t* __restrict__ codes, int64_t wbase,
+                                        const uint32_t (&part)[VPL], int lane) {
+  constexpr int E = IO::kPerVec;
+  constexpr int G = 16 / E;
+  constexpr int PART = 2 * E;
+  static_assert(VPL == 1 || VPL % G == 0, "VPL must be 1 or a multiple of the lane group");
+  const int q = lane % G;
+  if constexpr (VPL == 1) {
+    uint32_t word = part[0] << (q * PART);
+    word |= group_rotate<G, 1>(word);
+    if constexpr (G == 4) word |= group_rotate<4, 2>(word);
+    if (q == 0) {
+      if constexpr (kActNtCodeStore) __builtin_nontemporal_store(word, codes + wbase + lane / G);
+      else codes[wbase + lane / G] = word;
+    }
+  } else {
+#pragma unroll
+    for (int m = 0; m < VPL / G; ++m) {
+      uint32_t packed = 0;
+#pragma unroll
+      for (int t = 0; t < G; ++t) packed |= part[G * m + t] << (t * PART);
+      uint32_t word = 0;
+#pragma unroll
+      for (int s = 0; s < G; ++s) {
+        const uint32_t send = __builtin_amdgcn_alignbit(packed, packed, uint32_t(((q - s + G) % G) * PART));
+        uint32_t recv;
+        if constexpr (G == 2) {
+          recv = (s == 0) ? send : group_rotate<2, 1>(send);
+        } else {
+          recv = (s == 0) ? send : (s == 1) ? group_rotate<4, 1>(send)
+               : (s == 2) ? group_rotate<4, 2>(send) : group_rotate<4, 3>(send);
+        }
+        const uint32_t mask = (PART == 32) ? 0xffffffffu : ((1u << PART) - 1u);
+        word |= (recv & mask) << (((q + s) % G) * PART);
+      }
+      uint32_t* cw = codes + wbase + int64_t(G * m + q) * (kWave / G) + lane / G;
+      if constexpr (kActNtCodeStore) __builtin_nontemporal_store(word, cw);
+      else *cw = word;
+    }
+  }
+}
+
+// Load, for each of this lane's VPL vectors, the code bits of that vector (the
+// word shared by the lane group, shifted to this lane's part).
+template <class IO, int VPL>
+__device__ inline void load_tile_codes(const uint32_t* __restrict__ codes, int64_t wbase,
+                                       uint32_t (&part)[VPL], int lane) {
+  constexpr int G = 16 / IO::kPerVec;
+  constexpr int PART = 2 * IO::kPerVec;
+#pragma unroll
+  for (int j = 0; j < VPL; ++j) {
+    const uint32_t* cw = codes + wbase + j * (kWave / G) + lane / G;
+    uint32_t w;
+    if constexpr (kActNtCodeLoad) w = __builtin_nontemporal_load(cw);
+    else w = *cw;
+    part[j] = w >> ((lane % G) * PART);
+  }
+}
+
 // -------------------------------------------------------------------- kernels
 template <class IO, int ACT, int VPL>
 __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_fwd_kernel(const void* x, void* y,
@@ -184,10 +253,7 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_fwd_kernel(const void* x, 
   using A = ActOf<ACT>;
   constexpr bool kPrecise = std::is_same<IO, F32>::value;
   constexpr int E = IO::kPerVec;      // elements per 16-byte vector
-  constexpr int G = 16 / E;           // lanes sharing one code word
-  constexpr int PART = 2 * E;         // code bits per vector
   constexpr int TILE = kWave * VPL * E;
-  static_assert(VPL == 1 || VPL % G == 0, "VPL must be 1 or a multiple of the lane group");
 
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
@@ -215,46 +281,7 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_fwd_kernel(const void* x, 
       stg16<kActNtStore>(y, vbase + j * kWave + lane, IO::pack(o));
     }
 
-    const int q = lane % G;
-    const int64_t wbase = base / 16;
-    if constexpr (VPL == 1) {
-      // One vector per lane: the G lanes of a group hold consecutive parts of one
-      // word. Each shifts its part into place and the group ORs them together (one
-      // or two DPP steps); the group's first lane stores the word.
-      uint32_t word = part[0] << (q * PART);
-      word |= group_rotate<G, 1>(word);
-      if constexpr (G == 4) word |= group_rotate<4, 2>(word);
-      if (q == 0) {
-        if constexpr (kActNtCodeStore) __builtin_nontemporal_store(word, codes + wbase + lane / G);
-        else codes[wbase + lane / G] = word;
-      }
-      return;
-    }
-#pragma unroll
-    for (int m = 0; m < VPL / G; ++m) {
-      uint32_t packed = 0;
-#pragma unroll
-      for (int t = 0; t < G; ++t) packed |= part[G * m + t] << (t * PART);
-      // Step s: lane q sends part (q - s) mod G and receives, from lane (q + s) mod G,
-      // that lane's part for vector G*m + q.
-      uint32_t word = 0;
-#pragma unroll
-      for (int s = 0; s < G; ++s) {
-        const uint32_t send = __builtin_amdgcn_alignbit(packed, packed, uint32_t(((q - s + G) % G) * PART));
-        uint32_t recv;
-        if constexpr (G == 2) {
-          recv = (s == 0) ? send : group_rotate<2, 1>(send);
-        } else {
-          recv = (s == 0) ? send : (s == 1) ? group_rotate<4, 1>(send)
-               : (s == 2) ? group_rotate<4, 2>(send) : group_rotate<4, 3>(send);
-        }
-        const uint32_t mask = (PART == 32) ? 0xffffffffu : ((1u << PART) - 1u);
-        word |= (recv & mask) << (((q + s) % G) * PART);
-      }
-      uint32_t* cw = codes + wbase + int64_t(G * m + q) * (kWave / G) + lane / G;
-      if constexpr (kActNtCodeStore) __builtin_nontemporal_store(word, cw);
-      else *cw = word;
-    }
+    store_tile_codes<IO, VPL>(codes, base / 16, part, lane);
     return;
   }
 
@@ -281,8 +308,6 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_bwd_kernel(const void* dy,
                                                       void* dx, int64_t n, int vec_ok) {
   using A = ActOf<ACT>;
   constexpr int E = IO::kPerVec;
-  constexpr int G = 16 / E;
-  constexpr int PART = 2 * E;
   constexpr int TILE = kWave * VPL * E;
 
   const int lane = threadIdx.x & (kWave - 1);
@@ -294,17 +319,13 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_bwd_kernel(const void* dy,
     const int64_t vbase = base / E;
     const int64_t wbase = base / 16;
     u32x4 in[VPL];
-    uint32_t word[VPL];
+    uint32_t part[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) in[j] = ldg16<kActNtLoad>(dy, vbase + j * kWave + lane);
+    load_tile_codes<IO, VPL>(codes, wbase, part, lane);
 #pragma unroll
     for (int j = 0; j < VPL; ++j) {
-      in[j] = ldg16<kActNtLoad>(dy, vbase + j * kWave + lane);
-      const uint32_t* cw = codes + wbase + j * (kWave / G) + lane / G;
-      if constexpr (kActNtCodeLoad) word[j] = __builtin_nontemporal_load(cw);
-      else word[j] = *cw;
-    }
-#pragma unroll
-    for (int j = 0; j < VPL; ++j) {
-      const uint32_t p = word[j] >> ((lane % G) * PART);
+      const uint32_t p = part[j];
       float f[E];
       IO::unpack(in[j], f);
 #pragma unroll
@@ -318,6 +339,124 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_bwd_kernel(const void* dy,
   for (int64_t i = base + lane; i < end; i += kWave) {
     const uint32_t c = (codes[i / 16] >> (2 * (i % 16))) & 3u;
     IO::store1(dx, i, IO::load1(dy, i) * seg_slope<A>(c));
+  }
+}
+
+// ReSiLU2 (or ReGELU2) inside a gated product h = act(g) * u (SwiGLU when act is
+// SiLU). Forward writes h, s = act(g) (what the product's backward needs) and the
+// codes of g; backward: dg = dh * u * slope[code], du = dh * s. Same tiling as the
+// plain activation kernels; fusing saves the round trip of s and ds through HBM.
+template <class IO, int ACT, int VPL>
+__global__ __launch_bounds__(LMBP_ACT_BLOCK) void glu_fwd_kernel(const void* g, const void* u, void* h,
+                                                                 void* s, uint32_t* __restrict__ codes,
+                                                                 int64_t n, int vec_ok) {
+  using A = ActOf<ACT>;
+  constexpr bool kPrecise = std::is_same<IO, F32>::value;
+  constexpr int E = IO::kPerVec;
+  constexpr int TILE = kWave * VPL * E;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  const int64_t base = wave * TILE;
+  if (base >= n) return;
+
+  if (vec_ok && base + TILE <= n) {
+    const int64_t vbase = base / E;
+    u32x4 vg[VPL], vu[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      vg[j] = ldg16<kActNtLoad>(g, vbase + j * kWave + lane);
+      vu[j] = ldg16<kActNtLoad>(u, vbase + j * kWave + lane);
+    }
+    uint32_t part[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      float fg[E], fu[E], fs[E];
+      IO::unpack(vg[j], fg);
+      IO::unpack(vu[j], fu);
+      uint32_t p = 0;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        fs[e] = act_value<ACT, kPrecise>(fg[e]);
+        fu[e] = fs[e] * fu[e];
+        p |= seg_code<A>(fg[e]) << (2 * e);
+      }
+      part[j] = p;
+      stg16<kActNtStore>(s, vbase + j * kWave + lane, IO::pack(fs));
+      stg16<kActNtStore>(h, vbase + j * kWave + lane, IO::pack(fu));
+    }
+    store_tile_codes<IO, VPL>(codes, base / 16, part, lane);
+    return;
+  }
+
+  const int64_t end = (base + TILE < n) ? base + TILE : n;
+  const int64_t w_end = (end + 15) / 16;
+  for (int64_t w = base / 16 + lane; w < w_end; w += kWave) {
+    uint32_t word = 0;
+    for (int e = 0; e < 16; ++e) {
+      const int64_t i = w * 16 + e;
+      if (i < n) {
+        const float gv = IO::load1(g, i);
+        const float uv = IO::load1(u, i);
+        const float sv = act_value<ACT, kPrecise>(gv);
+        IO::store1(s, i, sv);
+        IO::store1(h, i, sv * uv);
+        word |= seg_code<A>(gv) << (2 * e);
+      }
+    }
+    codes[w] = word;
+  }
+}
+
+template <class IO, int ACT, int VPL>
+__global__ __launch_bounds__(LMBP_ACT_BLOCK) void glu_bwd_kernel(const void* dh, const void* u,
+                                                                 const void* s,
+                                                                 const uint32_t* __restrict__ codes,
+                                                                 void* dg, void* du, int64_t n,
+                                                                 int vec_ok) {
+  using A = ActOf<ACT>;
+  constexpr int E = IO::kPerVec;
+  constexpr int TILE = kWave * VPL * E;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
+  const int64_t base = wave * TILE;
+  if (base >= n) return;
+
+  if (vec_ok && base + TILE <= n) {
+    const int64_t vbase = base / E;
+    u32x4 vh[VPL], vu[VPL], vs[VPL];
+    uint32_t part[VPL];
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      vh[j] = ldg16<kActNtLoad>(dh, vbase + j * kWave + lane);
+      vu[j] = ldg16<kActNtLoad>(u, vbase + j * kWave + lane);
+      vs[j] = ldg16<kActNtLoad>(s, vbase + j * kWave + lane);
+    }
+    load_tile_codes<IO, VPL>(codes, base / 16, part, lane);
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      float fh[E], fu[E], fs[E];
+      IO::unpack(vh[j], fh);
+      IO::unpack(vu[j], fu);
+      IO::unpack(vs[j], fs);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        fu[e] = fh[e] * fu[e] * seg_slope<A>((part[j] >> (2 * e)) & 3u);   // dg
+        fs[e] = fh[e] * fs[e];                                              // du
+      }
+      stg16<kActNtStore>(dg, vbase + j * kWave + lane, IO::pack(fu));
+      stg16<kActNtStore>(du, vbase + j * kWave + lane, IO::pack(fs));
+    }
+    return;
+  }
+
+  const int64_t end = (base + TILE < n) ? base + TILE : n;
+  for (int64_t i = base + lane; i < end; i += kWave) {
+    const uint32_t c = (codes[i / 16] >> (2 * (i % 16))) & 3u;
+    const float hv = IO::load1(dh, i);
+    const float uv = IO::load1(u, i);
+    const float sv = IO::load1(s, i);
+    IO::store1(dg, i, hv * uv * seg_slope<A>(c));
+    IO::store1(du, i, hv * sv);
   }
 }
 
@@ -358,6 +497,41 @@ hipError_t launch_act_bwd_t(int64_t n, const void* dy, const uint32_t* codes, vo
   hipLaunchKernelGGL((act_bwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)), dim3(LMBP_ACT_BLOCK), 0, s,
                      dy, codes, dx, n, int(vec_ok));
   return hipGetLastError();
+}
+
+template <class IO, int ACT>
+hipError_t launch_glu_fwd_t(int64_t n, const void* g, const void* u, void* h, void* s,
+                            uint32_t* codes, bool vec_ok, hipStream_t st) {
+  const int64_t blocks = act_blocks<IO>(n);
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((glu_fwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)),
+                     dim3(LMBP_ACT_BLOCK), 0, st, g, u, h, s, codes, n, int(vec_ok));
+  return hipGetLastError();
+}
+
+template <class IO, int ACT>
+hipError_t launch_glu_bwd_t(int64_t n, const void* dh, const void* u, const void* s,
+                            const uint32_t* codes, void* dg, void* du, bool vec_ok, hipStream_t st) {
+  const int64_t blocks = act_blocks<IO>(n);
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  hipLaunchKernelGGL((glu_bwd_kernel<IO, ACT, act_vpl<IO>()>), dim3(unsigned(blocks)),
+                     dim3(LMBP_ACT_BLOCK), 0, st, dh, u, s, codes, dg, du, n, int(vec_ok));
+  return hipGetLastError();
+}
+
+hipError_t launch_glu_fwd(int act, bool bf16, int64_t n, const void* g, const void* u, void* h,
+                          void* s, uint32_t* codes, bool vec_ok, hipStream_t st) {
+  if (act != kSilu) return hipErrorInvalidValue;
+  return bf16 ? launch_glu_fwd_t<BF16, kSilu>(n, g, u, h, s, codes, vec_ok, st)
+              : launch_glu_fwd_t<F32, kSilu>(n, g, u, h, s, codes, vec_ok, st);
+}
+
+hipError_t launch_glu_bwd(int act, bool bf16, int64_t n, const void* dh, const void* u,
+                          const void* s, const uint32_t* codes, void* dg, void* du, bool vec_ok,
+                          hipStream_t st) {
+  if (act != kSilu) return hipErrorInvalidValue;
+  return bf16 ? launch_glu_bwd_t<BF16, kSilu>(n, dh, u, s, codes, dg, du, vec_ok, st)
+              : launch_glu_bwd_t<F32, kSilu>(n, dh, u, s, codes, dg, du, vec_ok, st);
 }
 
 hipError_t launch_act_fwd(int act, bool bf16, int64_t n, const void* x, void* y,

@@ -77,6 +77,55 @@ lmbp_status act_bwd(int act, lmbp_dtype dt, int64_t n, const void* dy, const uin
                                        static_cast<hipStream_t>(stream)));
 }
 
+lmbp_status glu_fwd(lmbp_dtype dt, int64_t n, const void* g, const void* u, void* h, void* s,
+                    uint32_t* codes, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (n < 0 || uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (n == 0) return LMBP_OK;
+  if (!g || !u || !h || !s || !codes) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(g, eb) || !aligned(u, eb) || !aligned(h, eb) || !aligned(s, eb) || !aligned(codes, 4))
+    return LMBP_EINVAL;
+  const uint64_t b = uint64_t(n) * eb;
+  const Span sg = span(g, b), su = span(u, b), sh = span(h, b), ss = span(s, b);
+  const Span sc = span(codes, lmbp_codes_bytes(n));
+  // h may replace g or u in place; s and codes overlap nothing.
+  if (bad_pair(sg, su, false) || bad_pair(sh, sg, true) || bad_pair(sh, su, true) ||
+      bad_pair(ss, sg, false) || bad_pair(ss, su, false) || bad_pair(ss, sh, false) ||
+      bad_pair(sc, sg, false) || bad_pair(sc, su, false) || bad_pair(sc, sh, false) ||
+      bad_pair(sc, ss, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(g, 16) && aligned(u, 16) && aligned(h, 16) && aligned(s, 16);
+  return from_hip(lmbp::launch_glu_fwd(lmbp::kSilu, dt == LMBP_BF16, n, g, u, h, s, codes, vec_ok,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+lmbp_status glu_bwd(lmbp_dtype dt, int64_t n, const void* dh, const void* u, const void* s,
+                    const uint32_t* codes, void* dg, void* du, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (n < 0 || uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (n == 0) return LMBP_OK;
+  if (!dh || !u || !s || !codes || !dg || !du) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(dh, eb) || !aligned(u, eb) || !aligned(s, eb) || !aligned(dg, eb) ||
+      !aligned(du, eb) || !aligned(codes, 4))
+    return LMBP_EINVAL;
+  const uint64_t b = uint64_t(n) * eb;
+  const Span sh = span(dh, b), su = span(u, b), ss = span(s, b), sg = span(dg, b), sd = span(du, b);
+  const Span sc = span(codes, lmbp_codes_bytes(n));
+  // dg may replace dh and du may replace u in place; nothing else overlaps.
+  if (bad_pair(sh, su, false) || bad_pair(sh, ss, false) || bad_pair(su, ss, false) ||
+      bad_pair(sg, sh, true) || bad_pair(sg, su, false) || bad_pair(sg, ss, false) ||
+      bad_pair(sd, su, true) || bad_pair(sd, sh, false) || bad_pair(sd, ss, false) ||
+      bad_pair(sd, sg, false) || bad_pair(sc, sh, false) || bad_pair(sc, su, false) ||
+      bad_pair(sc, ss, false) || bad_pair(sc, sg, false) || bad_pair(sc, sd, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(dh, 16) && aligned(u, 16) && aligned(s, 16) && aligned(dg, 16) &&
+                      aligned(du, 16);
+  return from_hip(lmbp::launch_glu_bwd(lmbp::kSilu, dt == LMBP_BF16, n, dh, u, s, codes, dg, du,
+                                       vec_ok, static_cast<hipStream_t>(stream)));
+}
+
 lmbp_status norm_fwd(bool ln, lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x,
                      void* z, float* rstd, void* stream) {
   if (!known_dtype(dt)) return LMBP_EDTYPE;
@@ -154,6 +203,15 @@ lmbp_status resilu2_fwd(lmbp_dtype dt, int64_t n, const void* x, void* y, uint32
 lmbp_status resilu2_bwd(lmbp_dtype dt, int64_t n, const void* dy, const uint32_t* codes, void* dx,
                         void* stream) {
   return act_bwd(lmbp::kSilu, dt, n, dy, codes, dx, stream);
+}
+
+lmbp_status reswiglu2_fwd(lmbp_dtype dt, int64_t n, const void* g, const void* u, void* h, void* s,
+                          uint32_t* codes, void* stream) {
+  return glu_fwd(dt, n, g, u, h, s, codes, stream);
+}
+lmbp_status reswiglu2_bwd(lmbp_dtype dt, int64_t n, const void* dh, const void* u, const void* s,
+                          const uint32_t* codes, void* dg, void* du, void* stream) {
+  return glu_bwd(dt, n, dh, u, s, codes, dg, du, stream);
 }
 
 lmbp_status msln_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x, void* z,

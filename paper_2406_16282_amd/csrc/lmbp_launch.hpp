@@ -13,6 +13,13 @@ hipError_t launch_act_fwd(int act, bool bf16, int64_t n, const void* x, void* y,
 hipError_t launch_act_bwd(int act, bool bf16, int64_t n, const void* dy, const uint32_t* codes,
                           void* dx, bool vec_ok, hipStream_t s);
 
+// Gated form h = act(g) * u (only act = kSilu is instantiated).
+hipError_t launch_glu_fwd(int act, bool bf16, int64_t n, const void* g, const void* u, void* h,
+                          void* s, uint32_t* codes, bool vec_ok, hipStream_t st);
+hipError_t launch_glu_bwd(int act, bool bf16, int64_t n, const void* dh, const void* u,
+                          const void* s, const uint32_t* codes, void* dg, void* du, bool vec_ok,
+                          hipStream_t st);
+
 // vec_ok: every tensor pointer 16-byte aligned and cols * element bytes a
 // multiple of 16 (each row starts on a vector boundary).
 hipError_t launch_norm_fwd(bool ln, bool bf16, int64_t rows, int64_t cols, float eps,

@@ -8,7 +8,8 @@ Recipe: ``numpy.random.Generator(PCG64(SeedSequence([seed, block, tensor_id])))`
 ``standard_normal`` in float64, scaled, rounded to fp32 (round to nearest even),
 then for bf16 rounded again from the fp32 bits to 16 bits (round to nearest even).
 tensor_id: 0 = norm input x, 1 = norm upstream gradient dz, 2 = activation input
-x, 3 = activation upstream gradient dy.
+x (the gate g of a SwiGLU product), 3 = activation upstream gradient dy (dh),
+4 = the SwiGLU "up" input u, drawn N(0, 1).
 
 The workloads mirror the activation shapes of the paper's fine-tuning runs
 (ViT-B/16 at 224 px: 197 tokens, width 768, MLP 3072; LLaMA-7B: width 4096,
@@ -21,7 +22,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 SEED = 0
-NORM_X, NORM_DZ, ACT_X, ACT_DY = 0, 1, 2, 3
+NORM_X, NORM_DZ, ACT_X, ACT_DY, ACT_U = 0, 1, 2, 3, 4
 
 
 def rng(seed, block, tensor_id):
@@ -182,6 +183,11 @@ class Workload:
     def act_dy(self, block=0, seed=SEED):
         s = self.act
         return normal((s.rows, s.cols), s.dy_std, s.dtype, seed, block, ACT_DY)
+
+    def act_u(self, block=0, seed=SEED):
+        """The "up" projection u of a SwiGLU product h = SiLU(g) * u (same shape as g)."""
+        s = self.act
+        return normal((s.rows, s.cols), 1.0, s.dtype, seed, block, ACT_U)
 
 
 WORKLOADS = {

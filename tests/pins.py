@@ -366,3 +366,36 @@ def pin_bf16_rounding(round_to_dtype, seed=0):
     vals += [2.0 ** -133 * 0.5, 2.0 ** -133 * 1.5, 1e-40, 3.0, 1e4, -1e4]
     got = round_to_dtype(np.array(vals), "bf16")
     return sum(int(_exact_bf16_round(v) != float(r)) for v, r in zip(vals, got))
+
+
+# ----------------------------------------------------------------- SwiGLU
+
+def pin_swiglu_fd(fwd, bwd, relu_combination, a, c, seed=5):
+    """Backward of h = SiLU(g) * u under Approx-BP against finite differences of the
+    approximate network h~(g) * u for dg (away from kinks) and of the exact product
+    in u for du (where du/du of s * u is s). Returns the worse absolute error."""
+    g = _kink_free_points(c, 800, seed)
+    r = np.random.default_rng(seed + 1)
+    u = r.normal(size=g.size)
+    dh = r.normal(size=g.size)
+    h, s, words = fwd(g, u)
+    dg, du = bwd(dh, u, s, words)
+    eps = 1e-6
+    fd_g = (relu_combination(g + eps, a, c) * u - relu_combination(g - eps, a, c) * u) / (2 * eps)
+    s_ref = F.silu(torch.from_numpy(g)).numpy()                   # SiLU from another library
+    fd_u = (s_ref * (u + eps) - s_ref * (u - eps)) / (2 * eps)
+    return max(float(np.max(np.abs(dg - dh * fd_g))), float(np.max(np.abs(du - dh * fd_u))))
+
+
+def pin_swiglu_reduces_to_resilu2(fwd, bwd, act_fwd, act_bwd, seed=6):
+    """With u = 1 the fused op is ReSiLU2 itself: h = s = SiLU(g), same codes, dg = ReSiLU2's dx."""
+    g = np.random.default_rng(seed).normal(0, 3, size=777)
+    one = np.ones_like(g)
+    dh = np.random.default_rng(seed + 1).normal(size=g.size)
+    h, s, words = fwd(g, one)
+    y, w2 = act_fwd(g)
+    dg, du = bwd(dh, one, s, words)
+    bad = int(not np.array_equal(words, w2))
+    err = max(float(np.max(np.abs(h - y))), float(np.max(np.abs(s - y))),
+              float(np.max(np.abs(dg - act_bwd(dh, w2)))), float(np.max(np.abs(du - dh * y))))
+    return bad + err

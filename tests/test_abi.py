@@ -34,7 +34,7 @@ def L():
 
 def test_every_declared_symbol_is_exported(L):
     names = declared_functions()
-    assert set(B.ACT_OPS + B.NORM_OPS) <= set(names)
+    assert set(B.ACT_OPS + B.NORM_OPS + B.GLU_OPS) <= set(names)
     for name in names:
         assert hasattr(L, name), name
 
@@ -102,6 +102,27 @@ def test_norm_bwd_errors(L, op):
     assert f(B.FP32, 4, 8, dz, z, r, z, s) == B.EOVERLAP          # dx on z is not allowed
     assert f(B.FP32, 4, 8, dz, z, r, dz + 4, s) == B.EOVERLAP     # partial overlap with dz
     assert f(B.FP32, 4, 8, dz, z, dz + 16, dx, s) == B.EOVERLAP   # rstd inside dz
+
+
+def test_swiglu_errors(L):
+    f, b = L.reswiglu2_fwd, L.reswiglu2_bwd
+    g, u, h, s, c = P, P + 4096, P + 8192, P + 12288, P + 16384
+    assert f(5, 16, g, u, h, s, c, None) == B.EDTYPE
+    assert f(B.BF16, -1, g, u, h, s, c, None) == B.EINVAL
+    assert f(B.BF16, 0, g, u, h, s, c, None) == B.OK
+    assert f(B.BF16, 16, g, u, h, None, c, None) == B.EINVAL
+    assert f(B.BF16, 16, g + 1, u, h, s, c, None) == B.EINVAL
+    assert f(B.BF16, 16, g, g + 8, h, s, c, None) == B.EOVERLAP    # g and u overlap
+    assert f(B.BF16, 16, g, u, h, g, c, None) == B.EOVERLAP        # s on an input
+    assert f(B.BF16, 16, g, u, h, s, s + 4, None) == B.EOVERLAP    # codes inside s
+    assert f(B.BF16, 16, g, u, h, h + 2, c, None) == B.EOVERLAP    # s overlaps h
+    dh, dg, du = P, P + 20480, P + 24576
+    assert b(B.BF16, -3, dh, u, s, c, dg, du, None) == B.EINVAL
+    assert b(B.BF16, 16, dh, u, s, c, dg, None, None) == B.EINVAL
+    assert b(B.BF16, 16, dh, u, s, c, s, du, None) == B.EOVERLAP      # dg on s
+    assert b(B.BF16, 16, dh, u, s, c, dg, dh, None) == B.EOVERLAP     # du on dh
+    assert b(B.BF16, 16, dh, u, s, c, dg, dg, None) == B.EOVERLAP     # dg and du alias
+    assert b(B.BF16, 16, dh, u, s, dg + 4, dg, du, None) == B.EOVERLAP
 
 
 def test_copy_errors(L):

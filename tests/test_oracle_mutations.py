@@ -157,3 +157,19 @@ def test_bf16_truncation_caught():
         x = np.asarray(x, dtype=np.float64).astype(np.float32)
         return ((x.view(np.uint32) & np.uint32(0xFFFF0000)).view(np.float32)).astype(np.float64)
     assert pins.pin_bf16_rounding(trunc) > 0
+
+
+def test_swiglu_du_from_codes_instead_of_s_caught():
+    def bad_bwd(dh, u, s, words):
+        dg, du = oracle.reswiglu2_bwd(dh, u, s, words)
+        return dg, dh * u   # product rule with the wrong factor
+    assert pins.pin_swiglu_fd(oracle.reswiglu2_fwd, bad_bwd, oracle.relu_combination,
+                              oracle.SILU_A, oracle.SILU_C) > 1e-2
+
+
+def test_swiglu_dg_without_u_caught():
+    def bad_bwd(dh, u, s, words):
+        dg, du = oracle.reswiglu2_bwd(dh, np.ones_like(u), s, words)
+        return dg, dh * s
+    assert pins.pin_swiglu_fd(oracle.reswiglu2_fwd, bad_bwd, oracle.relu_combination,
+                              oracle.SILU_A, oracle.SILU_C) > 1e-2
