@@ -1,0 +1,115 @@
+"""Autograd modules over the kernels, checked against the CPU oracle on the GPU."""
+
+import numpy as np
+import pytest
+import torch
+from torch import nn
+
+import oracle
+from paper_2406_16282_amd import inputs
+from paper_2406_16282_amd.nn import (MSLayerNorm, MSRMSNorm, ReGELU2, ReSiLU2, ReSwiGLU2,
+                                     merge_norm_into_linears)
+from compare import assert_codes_equal, assert_mixed, assert_rel
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def T(a, grad=False):
+    t = inputs.storage_to_torch(a, DEV)
+    return t.requires_grad_(grad)
+
+
+def H(t):
+    return inputs.torch_to_storage(t)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("which", ["gelu", "silu"])
+def test_activation_modules(which, dtype):
+    shape = (64, 3072)
+    x = inputs.normal(shape, 2.0, dtype, tensor_id=inputs.ACT_X)
+    dy = inputs.normal(shape, 1.0, dtype, tensor_id=inputs.ACT_DY)
+    xt = T(x, True)
+    y = (ReGELU2() if which == "gelu" else ReSiLU2())(xt)
+    y.backward(T(dy))
+    fwd = oracle.regelu2_fwd if which == "gelu" else oracle.resilu2_fwd
+    bwd = oracle.regelu2_bwd if which == "gelu" else oracle.resilu2_bwd
+    y_o, w_o = fwd(oracle.decode(x, dtype))
+    rtol = 1e-5 if dtype == "fp32" else 1e-2
+    assert_rel(oracle.decode(H(y), dtype), y_o, rtol, "module y")
+    assert_rel(oracle.decode(H(xt.grad), dtype), bwd(oracle.decode(dy, dtype), w_o), rtol, "module dx", floor=0.0)
+
+
+def test_swiglu_module():
+    shape = (32, 11008)
+    g = inputs.normal(shape, 2.0, "bf16", tensor_id=inputs.ACT_X)
+    u = inputs.normal(shape, 1.0, "bf16", tensor_id=inputs.ACT_U)
+    dh = inputs.normal(shape, 1.0, "bf16", tensor_id=inputs.ACT_DY)
+    gt, ut = T(g, True), T(u, True)
+    h = ReSwiGLU2()(gt, ut)
+    h.backward(T(dh))
+    h_o, s_o, w_o = oracle.reswiglu2_fwd(oracle.decode(g, "bf16"), oracle.decode(u, "bf16"))
+    # the backward sees the stored s (bf16), as the module saves it
+    dg_o, du_o = oracle.reswiglu2_bwd(oracle.decode(dh, "bf16"), oracle.decode(u, "bf16"),
+                                      oracle.round_to_dtype(s_o, "bf16"), w_o)
+    assert_rel(oracle.decode(H(h), "bf16"), h_o, 2e-2, "swiglu h")
+    assert_rel(oracle.decode(H(gt.grad), "bf16"), dg_o, 2e-2, "swiglu dg", floor=0.0)
+    assert_rel(oracle.decode(H(ut.grad), "bf16"), du_o, 2e-2, "swiglu du", floor=0.0)
+
+
+@pytest.mark.parametrize("kind", ["ln", "rms"])
+def test_merged_norm_linear_against_oracle(kind):
+    """LayerNorm/RMSNorm with affine followed by two linear layers, merged, run through the
+    MS norm kernel and torch linears in fp32; compared with the oracle norm composed with
+    the same merged weights in fp64, forward and input gradient."""
+    torch.manual_seed(0)
+    rows, p = 96, 768
+    norm = (nn.LayerNorm(p, eps=1e-6) if kind == "ln" else nn.RMSNorm(p, eps=1e-5)).to(DEV)
+    with torch.no_grad():
+        norm.weight.copy_(1 + 0.2 * torch.randn(p))
+        if kind == "ln":
+            norm.bias.copy_(0.2 * torch.randn(p))
+    lins = [nn.Linear(p, 256).to(DEV), nn.Linear(p, 64).to(DEV)]
+    x = inputs.normal((rows, p), 1.5, "fp32", tensor_id=inputs.NORM_X)
+    dys = [inputs.normal((rows, l.out_features), 1.0, "fp32", tensor_id=10 + k) for k, l in enumerate(lins)]
+    ms = merge_norm_into_linears(norm, lins)
+    xt = T(x, True)
+    z = ms(xt)
+    ys = [l(z) for l in lins]
+    sum((y * T(d)).sum() for y, d in zip(ys, dys)).backward()
+
+    ofwd = oracle.msln_fwd if kind == "ln" else oracle.msrms_fwd
+    obwd = oracle.msln_bwd if kind == "ln" else oracle.msrms_bwd
+    z_o, r_o = ofwd(x.astype(np.float64), float(np.float32(ms.eps)))
+    Ws = [l.weight.detach().cpu().double().numpy() for l in lins]
+    bs = [l.bias.detach().cpu().double().numpy() for l in lins]
+    for y, W, b in zip(ys, Ws, bs):
+        assert_mixed(H(y).astype(np.float64), z_o @ W.T + b, 1e-5, f"{kind} merged y")
+    dz_o = sum(d.astype(np.float64) @ W for d, W in zip(dys, Ws))
+    assert_mixed(H(xt.grad).astype(np.float64), obwd(dz_o, z_o, r_o), 1e-5, f"{kind} merged dx")
+
+
+def test_norm_saves_only_z_shared_with_the_linear_and_rstd():
+    """Memory sharing (Prop. 5.1): the tensors autograd saves for MS-LN followed by a
+    linear layer are z (saved once, by both), rstd and the weight."""
+    p = 512
+    ms, lin = MSLayerNorm(1e-6), nn.Linear(p, 128).to(DEV)
+    x = torch.randn(64, p, device=DEV, requires_grad=True)
+    saved = []
+    with torch.autograd.graph.saved_tensors_hooks(lambda t: (saved.append(t), t)[1], lambda t: t):
+        z = ms(x)
+        y = lin(z)
+    ptrs = {t.data_ptr(): t for t in saved}
+    act = [t for t in ptrs.values() if t.data_ptr() != lin.weight.data_ptr()]
+    assert sorted(tuple(t.shape) for t in act) == [(64,), (64, p)]
+    assert any(t.data_ptr() == z.data_ptr() for t in act)
+
+
+def test_activation_saves_only_codes():
+    x = torch.randn(256, 1024, device=DEV, dtype=torch.bfloat16, requires_grad=True)
+    saved = []
+    with torch.autograd.graph.saved_tensors_hooks(lambda t: (saved.append(t), t)[1], lambda t: t):
+        ReSiLU2()(x)
+    assert len(saved) == 1 and saved[0].dtype == torch.int32
+    assert saved[0].numel() * 4 == x.numel() // 4   # 2 bits per element
