@@ -9,6 +9,7 @@
  *   msln_fwd    / msln_bwd      MS-LN    (Sec. 5.2 Alg. 1; Appendix G Alg. 2)
  *   msrms_fwd   / msrms_bwd     MS-RMSNorm (Appendix G Alg. 3)
  *   reswiglu2_fwd / reswiglu2_bwd  ReSiLU2 fused with the SwiGLU product (LLaMA MLP)
+ *   stepact_fwd / stepact_bwd      k-bit family members with runtime tables (ReGELU2-d, ...)
  *
  * Conventions shared by every call
  * --------------------------------
@@ -114,6 +115,31 @@ lmbp_status reswiglu2_fwd(lmbp_dtype dt, int64_t n, const void *g, const void *u
 lmbp_status reswiglu2_bwd(lmbp_dtype dt, int64_t n, const void *dh, const void *u,
                           const void *s, const uint32_t *codes, void *dg, void *du,
                           void *stream);
+
+/* ------------------------------------------------------------------------
+ * General members of the ReLU-combination family (eq. relus_family with k bits;
+ * Appendix I's ReGELU2-d is k = 2 with other constants), with runtime tables.
+ *
+ * Forward: y = GELU(x) or SiLU(x) exactly (act), and the k-bit code of every
+ * element: the number of the 2^k - 1 thresholds strictly below x (the biases c of
+ * the combination). Backward: dx = dy * levels[code] (2^k levels: the slopes of the
+ * combination on its segments, cumulative sums of its weights).
+ *
+ *   bits       : k in {1, 2, 4}; codes hold 32/k elements per 32-bit word, least
+ *                significant first, zero tail; lmbp_stepact_codes_bytes(k, n) bytes.
+ *   thresholds : host array of 2^k - 1 finite, strictly increasing doubles (read
+ *                during the call only). Each is applied as an exact real comparison.
+ *   levels     : host array of 2^k finite doubles, used as fp32 values.
+ *   x, y, dy, dx, codes: as for regelu2_fwd / regelu2_bwd (y == x, dx == dy allowed).
+ * LMBP_EINVAL also for bad k, act, tables or a NULL table pointer.
+ * ------------------------------------------------------------------------ */
+typedef enum { LMBP_ACT_GELU = 0, LMBP_ACT_SILU = 1 } lmbp_act;
+
+size_t lmbp_stepact_codes_bytes(int bits, int64_t n);
+lmbp_status stepact_fwd(lmbp_act act, int bits, const double *thresholds, lmbp_dtype dt,
+                        int64_t n, const void *x, void *y, uint32_t *codes, void *stream);
+lmbp_status stepact_bwd(int bits, const double *levels, lmbp_dtype dt, int64_t n,
+                        const void *dy, const uint32_t *codes, void *dx, void *stream);
 
 /* ------------------------------------------------------------------------
  * MS-LN (Sec. 5.2 Alg. 1, Appendix G Alg. 2) and MS-RMSNorm (Alg. 3), for a

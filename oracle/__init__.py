@@ -13,6 +13,7 @@ What it computes, each function citing the passage it follows:
   ``dx = dy * (slope of the ReLU combination on the element's segment)``.
 * ``activations`` also holds ReSiLU2 inside a SwiGLU product (h = SiLU(g) * u), the
   form it takes in the LLaMA MLP.
+* ``variants``: the general k-bit family and Appendix I's ReGELU2-d constants.
 * ``norms``: MS-LN and MS-RMSNorm (Sec. 5.2 Alg. 1; Appendix G Alg. 2 and Alg. 3):
   forward ``z = H x / sigma`` saving ``z`` and ``1/sigma``; backward
   ``dx = sigma^-1 (H - p^-1 z z^T) dz`` from the saved output alone.
@@ -33,6 +34,7 @@ from .activations import (
     reswiglu2_fwd, reswiglu2_bwd,
 )
 from .norms import msln_fwd, msln_bwd, msrms_fwd, msrms_bwd
+from . import variants
 
 __all__ = [
     "decode", "encode", "round_to_dtype", "DTYPES",
@@ -41,5 +43,5 @@ __all__ = [
     "gelu", "silu", "pack_codes", "unpack_codes", "codes_words",
     "regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd",
     "reswiglu2_fwd", "reswiglu2_bwd",
-    "msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd",
+    "msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd", "variants",
 ]

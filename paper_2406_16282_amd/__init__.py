@@ -26,4 +26,6 @@ from .binding import (  # noqa: F401
     resilu2_fwd,
     reswiglu2_bwd,
     reswiglu2_fwd,
+    stepact_bwd,
+    stepact_fwd,
 )

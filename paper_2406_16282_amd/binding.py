@@ -21,6 +21,8 @@ OK, EINVAL, EDTYPE, EOVERLAP, EHIP = 0, 1, 2, 3, 4
 ACT_OPS = ("regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd")
 NORM_OPS = ("msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd")
 GLU_OPS = ("reswiglu2_fwd", "reswiglu2_bwd")
+STEP_OPS = ("stepact_fwd", "stepact_bwd")
+ACT_GELU, ACT_SILU = 0, 1
 
 
 class LmbpError(RuntimeError):
@@ -65,6 +67,13 @@ def lib():
     L.reswiglu2_fwd.restype = i32
     L.reswiglu2_bwd.argtypes = [i32, i64, vp, vp, vp, vp, vp, vp, vp]
     L.reswiglu2_bwd.restype = i32
+    dp = ctypes.POINTER(ctypes.c_double)
+    L.lmbp_stepact_codes_bytes.argtypes = [i32, i64]
+    L.lmbp_stepact_codes_bytes.restype = ctypes.c_size_t
+    L.stepact_fwd.argtypes = [i32, i32, dp, i32, i64, vp, vp, vp, vp]
+    L.stepact_fwd.restype = i32
+    L.stepact_bwd.argtypes = [i32, dp, i32, i64, vp, vp, vp, vp]
+    L.stepact_bwd.restype = i32
     L.lmbp_copy.argtypes = [vp, vp, i64, vp]
     L.lmbp_copy.restype = i32
     _lib = L
@@ -214,6 +223,46 @@ def reswiglu2_bwd(dh, u, s, codes, dg=None, du=None, stream=None):
     _check("reswiglu2_bwd", lib().reswiglu2_bwd(dt, dh.numel(), _ptr(dh), _ptr(u), _ptr(s), _ptr(codes),
                                                 _ptr(dg), _ptr(du), _stream(dh, stream)))
     return dg, du
+
+
+def _doubles(values, count, what):
+    vals = [float(v) for v in values]
+    if len(vals) != count:
+        raise ValueError(f"{what} needs {count} values, got {len(vals)}")
+    return (ctypes.c_double * count)(*vals)
+
+
+def stepact_fwd(x, act, thresholds, bits, y=None, codes=None, stream=None):
+    """k-bit family member: returns (act(x), k-bit codes). ``act`` is "gelu" or "silu";
+    ``thresholds`` are the 2^k - 1 increasing biases of the ReLU combination."""
+    _dev(x, "x")
+    dt = _dtype_code(x)
+    a = {"gelu": ACT_GELU, "silu": ACT_SILU}[act]
+    tab = _doubles(thresholds, (1 << bits) - 1, "thresholds")
+    y = _like(x, y, "y")
+    words = int(lib().lmbp_stepact_codes_bytes(bits, x.numel())) // 4
+    if codes is None:
+        codes = torch.empty(words, dtype=torch.int32, device=x.device)
+    elif codes.dtype != torch.int32 or codes.numel() < words or codes.device != x.device:
+        raise ValueError(f"codes must be an int32 GPU tensor of at least {words} words")
+    _check("stepact_fwd", lib().stepact_fwd(a, bits, tab, dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes),
+                                            _stream(x, stream)))
+    return y, codes
+
+
+def stepact_bwd(dy, codes, levels, bits, dx=None, stream=None):
+    """Backward of stepact_fwd: dx = dy * levels[code] (2^k levels)."""
+    _dev(dy, "dy")
+    dt = _dtype_code(dy)
+    _dev(codes, "codes")
+    words = int(lib().lmbp_stepact_codes_bytes(bits, dy.numel())) // 4
+    if codes.dtype != torch.int32 or codes.numel() < words:
+        raise ValueError("codes must be the int32 buffer written by the forward")
+    tab = _doubles(levels, 1 << bits, "levels")
+    dx = _like(dy, dx, "dx")
+    _check("stepact_bwd", lib().stepact_bwd(bits, tab, dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx),
+                                            _stream(dy, stream)))
+    return dx
 
 
 def _rows_cols(t):

@@ -7,6 +7,7 @@
 
 #include <cmath>
 #include <cstdint>
+#include <limits>
 
 namespace {
 
@@ -126,6 +127,72 @@ lmbp_status glu_bwd(lmbp_dtype dt, int64_t n, const void* dh, const void* u, con
                                        vec_ok, static_cast<hipStream_t>(stream)));
 }
 
+uint64_t step_codes_bytes(int bits, int64_t n) {
+  const uint64_t per = uint64_t(32 / bits);
+  return n <= 0 ? 0 : (uint64_t(n) + per - 1) / per * 4;
+}
+
+bool valid_bits(int bits) { return bits == 1 || bits == 2 || bits == 4; }
+
+// Largest fp32 value not above c (for finite c within the fp32 range).
+float round_down_f32(double c) {
+  float f = static_cast<float>(c);
+  if (static_cast<double>(f) > c) f = std::nextafter(f, -std::numeric_limits<float>::infinity());
+  return f;
+}
+
+lmbp_status stepact_fwd_impl(int act, int bits, const double* thresholds, lmbp_dtype dt, int64_t n,
+                             const void* x, void* y, uint32_t* codes, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (!valid_bits(bits) || (act != LMBP_ACT_GELU && act != LMBP_ACT_SILU)) return LMBP_EINVAL;
+  if (n < 0 || uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (!thresholds) return LMBP_EINVAL;
+  const int nt = (1 << bits) - 1;
+  lmbp::StepTable tab{};
+  for (int i = 0; i < nt; ++i) {
+    const double c = thresholds[i];
+    if (!std::isfinite(c) || std::fabs(c) > 3.0e38 || (i > 0 && !(c > thresholds[i - 1])))
+      return LMBP_EINVAL;
+    tab.t[i] = round_down_f32(c);
+  }
+  if (n == 0) return LMBP_OK;
+  if (!x || !y || !codes) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(x, eb) || !aligned(y, eb) || !aligned(codes, 4)) return LMBP_EINVAL;
+  const Span sx = span(x, uint64_t(n) * eb), sy = span(y, uint64_t(n) * eb);
+  const Span sc = span(codes, step_codes_bytes(bits, n));
+  if (bad_pair(sx, sy, true) || bad_pair(sc, sx, false) || bad_pair(sc, sy, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(x, 16) && aligned(y, 16);
+  return from_hip(lmbp::launch_stepact_fwd(act == LMBP_ACT_GELU ? lmbp::kGelu : lmbp::kSilu, bits,
+                                           dt == LMBP_BF16, n, x, y, codes, vec_ok, tab,
+                                           static_cast<hipStream_t>(stream)));
+}
+
+lmbp_status stepact_bwd_impl(int bits, const double* levels, lmbp_dtype dt, int64_t n, const void* dy,
+                             const uint32_t* codes, void* dx, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (!valid_bits(bits)) return LMBP_EINVAL;
+  if (n < 0 || uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (!levels) return LMBP_EINVAL;
+  lmbp::StepTable tab{};
+  for (int i = 0; i < (1 << bits); ++i) {
+    if (!std::isfinite(levels[i]) || std::fabs(levels[i]) > 3.0e38) return LMBP_EINVAL;
+    tab.lv[i] = static_cast<float>(levels[i]);
+  }
+  if (n == 0) return LMBP_OK;
+  if (!dy || !dx || !codes) return LMBP_EINVAL;
+  const int eb = elem_bytes(dt);
+  if (!aligned(dy, eb) || !aligned(dx, eb) || !aligned(codes, 4)) return LMBP_EINVAL;
+  const Span sg = span(dy, uint64_t(n) * eb), sd = span(dx, uint64_t(n) * eb);
+  const Span sc = span(codes, step_codes_bytes(bits, n));
+  if (bad_pair(sg, sd, true) || bad_pair(sc, sg, false) || bad_pair(sc, sd, false))
+    return LMBP_EOVERLAP;
+  const bool vec_ok = aligned(dy, 16) && aligned(dx, 16);
+  return from_hip(lmbp::launch_stepact_bwd(bits, dt == LMBP_BF16, n, dy, codes, dx, vec_ok, tab,
+                                           static_cast<hipStream_t>(stream)));
+}
+
 lmbp_status norm_fwd(bool ln, lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x,
                      void* z, float* rstd, void* stream) {
   if (!known_dtype(dt)) return LMBP_EDTYPE;
@@ -212,6 +279,18 @@ lmbp_status reswiglu2_fwd(lmbp_dtype dt, int64_t n, const void* g, const void* u
 lmbp_status reswiglu2_bwd(lmbp_dtype dt, int64_t n, const void* dh, const void* u, const void* s,
                           const uint32_t* codes, void* dg, void* du, void* stream) {
   return glu_bwd(dt, n, dh, u, s, codes, dg, du, stream);
+}
+
+size_t lmbp_stepact_codes_bytes(int bits, int64_t n) {
+  return valid_bits(bits) ? size_t(step_codes_bytes(bits, n)) : 0;
+}
+lmbp_status stepact_fwd(lmbp_act act, int bits, const double* thresholds, lmbp_dtype dt, int64_t n,
+                        const void* x, void* y, uint32_t* codes, void* stream) {
+  return stepact_fwd_impl(act, bits, thresholds, dt, n, x, y, codes, stream);
+}
+lmbp_status stepact_bwd(int bits, const double* levels, lmbp_dtype dt, int64_t n, const void* dy,
+                        const uint32_t* codes, void* dx, void* stream) {
+  return stepact_bwd_impl(bits, levels, dt, n, dy, codes, dx, stream);
 }
 
 lmbp_status msln_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps, const void* x, void* z,

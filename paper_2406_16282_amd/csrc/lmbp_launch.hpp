@@ -8,6 +8,13 @@ namespace lmbp {
 
 enum { kGelu = 0, kSilu = 1 };
 
+// Runtime tables of a general family member (kernel argument, passed by value):
+// thresholds t[0..2^k-2] as fp32 round-down values, levels lv[0..2^k-1] in fp32.
+struct StepTable {
+  float t[15];
+  float lv[16];
+};
+
 hipError_t launch_act_fwd(int act, bool bf16, int64_t n, const void* x, void* y,
                           uint32_t* codes, bool vec_ok, hipStream_t s);
 hipError_t launch_act_bwd(int act, bool bf16, int64_t n, const void* dy, const uint32_t* codes,
@@ -27,6 +34,11 @@ hipError_t launch_norm_fwd(bool ln, bool bf16, int64_t rows, int64_t cols, float
 hipError_t launch_norm_bwd(bool ln, bool bf16, int64_t rows, int64_t cols, const void* dz,
                            const void* z, const float* rstd, void* dx, bool vec_ok,
                            hipStream_t s);
+
+hipError_t launch_stepact_fwd(int act, int bits, bool bf16, int64_t n, const void* x, void* y,
+                              uint32_t* codes, bool vec_ok, const StepTable& tab, hipStream_t s);
+hipError_t launch_stepact_bwd(int bits, bool bf16, int64_t n, const void* dy, const uint32_t* codes,
+                              void* dx, bool vec_ok, const StepTable& tab, hipStream_t s);
 
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
 

@@ -143,3 +143,24 @@ def test_binding_rejects_cpu_tensors(L):
     import torch
     with pytest.raises(ValueError):
         lmbp.resilu2_fwd(torch.zeros(16, dtype=torch.bfloat16))
+
+
+def test_stepact_errors(L):
+    import ctypes
+    t3 = (ctypes.c_double * 3)(-1.0, 0.0, 1.0)
+    bad = (ctypes.c_double * 3)(-1.0, 1.0, 0.5)       # not increasing
+    nan = (ctypes.c_double * 3)(-1.0, float("nan"), 1.0)
+    lv4 = (ctypes.c_double * 4)(0.0, 0.2, 0.7, 1.0)
+    f, b = L.stepact_fwd, L.stepact_bwd
+    x, y, c = P, P + 4096, P + 8192
+    assert f(0, 2, t3, 7, 16, x, y, c, None) == B.EDTYPE
+    assert f(0, 3, t3, B.BF16, 16, x, y, c, None) == B.EINVAL     # k = 3 not supported
+    assert f(5, 2, t3, B.BF16, 16, x, y, c, None) == B.EINVAL     # unknown activation
+    assert f(0, 2, None, B.BF16, 16, x, y, c, None) == B.EINVAL
+    assert f(0, 2, bad, B.BF16, 16, x, y, c, None) == B.EINVAL
+    assert f(0, 2, nan, B.BF16, 16, x, y, c, None) == B.EINVAL
+    assert f(0, 2, t3, B.BF16, 0, x, y, c, None) == B.OK
+    assert f(0, 2, t3, B.BF16, 16, x, x + 2, c, None) == B.EOVERLAP
+    assert b(2, None, B.BF16, 16, x, c, y, None) == B.EINVAL
+    assert b(2, lv4, B.BF16, 16, x, x + 4, y, None) == B.EOVERLAP
+    assert [L.lmbp_stepact_codes_bytes(k, 33) for k in (1, 2, 3, 4)] == [8, 12, 0, 20]
