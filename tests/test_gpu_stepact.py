@@ -90,3 +90,14 @@ def test_module_regelu2_d_autograd():
     xs = x.detach().cpu().double().numpy()
     lv = OV.family_levels(OV.REGELU2D_A)[OV.family_code(xs, OV.REGELU2D_C)]
     assert np.allclose(x.grad.cpu().double().numpy(), lv, rtol=1e-6, atol=0)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_fitted_four_bit_gelu(dtype):
+    """A k = 4 member fitted by the offline search (15 biases, 16 slopes) through the kernels."""
+    from paper_2406_16282_amd import fit
+    a, c, _ = fit.fit("gelu", 4, starts=1)
+    shape = (128, 4096)
+    x = inputs.edge_activation(shape, dtype, list(c))
+    dy = inputs.normal(shape, 1.0, dtype, tensor_id=inputs.ACT_DY)
+    check("gelu", 4, list(a), list(c), dtype, x, dy, "fitted k=4")
