@@ -129,6 +129,42 @@ def edge_norm_rows(shape, dtype, seed=SEED, tensor_id=NORM_X):
     return to_storage(x, dtype)
 
 
+# ---------------------------------------------------------------- large tensors
+
+HASH_MUL = 2654435761  # Knuth's multiplicative hash constant
+
+
+def hash_values(index, scale=8.0, salt=0):
+    """Closed-form pseudo-random values for flat element indices (an integer hash of
+    index + salt mapped to [-scale, scale)), as float64. Used for tensors too large to
+    draw on the host: the device computes the same formula for every element, the host
+    only for the sampled indices it checks. Different salts give unrelated tensors."""
+    i = np.asarray(index, dtype=np.int64) + np.int64(salt)
+    hsh = (i * HASH_MUL) & 0xFFFFFFFF
+    return ((hsh >> 8).astype(np.float64) / float(1 << 24) * 2.0 - 1.0) * scale
+
+
+def hash_tensor(n, dtype, device, scale=8.0, salt=0, chunk=1 << 27):
+    """The values of ``hash_values(range(n), scale, salt)`` rounded to ``dtype``, built on
+    ``device`` with torch integer arithmetic in chunks (no host copy of the tensor)."""
+    import torch
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    out = torch.empty(n, dtype=tdt, device=device)
+    for s in range(0, n, chunk):
+        e = min(n, s + chunk)
+        i = torch.arange(s + salt, e + salt, dtype=torch.int64, device=device)
+        hsh = (i * HASH_MUL) & 0xFFFFFFFF
+        v = ((hsh >> 8).to(torch.float64) / float(1 << 24) * 2.0 - 1.0) * scale
+        out[s:e] = v.to(torch.float32).to(tdt)
+    return out
+
+
+def hash_storage(index, dtype, scale=8.0, salt=0):
+    """Host storage values (fp32 array or bf16 patterns) of ``hash_tensor`` at ``index``:
+    the same float64 -> fp32 -> dtype rounding chain."""
+    return to_storage(hash_values(index, scale, salt), dtype)
+
+
 # ---------------------------------------------------------------- workloads
 
 @dataclass(frozen=True)
