@@ -10,6 +10,13 @@ elementwise relative test cannot hold for outputs that cancel to nearly zero
 (norm outputs and gradients), even for an exact fp32 evaluation; the row scale is
 the natural size against which their rounding is measured.
 
+Norm backward: dx = rstd * (dz - mean(dz) - z * mean(z * dz)) (Alg. 2, Alg. 3) is a
+projection of rstd * dz, and its rounding is bounded relative to the size of the
+terms it combines, rstd * rms(dz), not relative to its result: for rows where the
+projection nearly annihilates dz (a LayerNorm row of two elements has z = +-1 up
+to eps, so dx is of order eps) the output RMS is no measure of the arithmetic.
+There s_row is max(rms(ref), rstd * rms(dz)) (``norm_grad_scale``).
+
 Strict rules (activations): the forward value is within rtol relative for every
 element with |ref| >= 2^-60 (below that the result is at the edge of the fp32
 range and only the mixed rule applies); the backward value is within rtol
@@ -30,11 +37,19 @@ def _rows2d(a):
     return a.reshape(1, -1) if a.ndim == 1 else a.reshape(-1, a.shape[-1])
 
 
-def assert_mixed(got, ref, rtol, what):
+def norm_grad_scale(dz, rstd):
+    """Per-row size rstd * rms(dz) of the terms of a norm backward."""
+    d = _rows2d(dz)
+    return np.asarray(rstd, dtype=np.float64).reshape(-1, 1) * np.sqrt(np.mean(d * d, axis=1, keepdims=True))
+
+
+def assert_mixed(got, ref, rtol, what, row_scale=None):
     g, r = _rows2d(got), _rows2d(ref)
     assert g.shape == r.shape, f"{what}: shape {g.shape} vs {r.shape}"
     assert np.all(np.isfinite(g)), f"{what}: non-finite values"
     s = np.sqrt(np.mean(r * r, axis=1, keepdims=True))
+    if row_scale is not None:
+        s = np.maximum(s, np.asarray(row_scale, dtype=np.float64).reshape(-1, 1))
     err = np.abs(g - r)
     lim = rtol * (np.abs(r) + s)
     bad = err > lim

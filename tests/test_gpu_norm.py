@@ -11,7 +11,7 @@ import torch
 import oracle
 import paper_2406_16282_amd as lmbp
 from paper_2406_16282_amd import inputs
-from compare import assert_mixed, assert_rel, rtol_for
+from compare import assert_mixed, assert_rel, norm_grad_scale, rtol_for
 
 pytestmark = pytest.mark.gpu
 
@@ -46,7 +46,8 @@ def check_norm(op, dtype, x, dz, eps, label):
 
     assert_mixed(oracle.decode(H(z), dtype), z_o, rtol, f"{label} z")
     assert_rel(H(rstd).astype(np.float64), r_o, 1e-5, f"{label} rstd", floor=0.0)
-    assert_mixed(oracle.decode(H(dx), dtype), dx_o, rtol, f"{label} dx")
+    assert_mixed(oracle.decode(H(dx), dtype), dx_o, rtol, f"{label} dx",
+                 row_scale=norm_grad_scale(oracle.decode(dz, dtype), r_saved))
     return z, rstd
 
 
