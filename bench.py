@@ -16,7 +16,11 @@ events on the kernels' stream). Per-kernel launch durations come from a second
 event-timed loop that launches each kernel back to back over rotating tensor
 sets; the dominant kernel's figure feeds the roofline entry.
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--swiglu] [--pairs]
+
+--pairs adds, for every workload (ViT-B fp32, ViT-B batch 64 bf16 x 12 blocks,
+LLaMA-7B and LLaMA-13B shapes), the forward + backward GB/s of the norm pair and
+of the activation pair, cold and warm.
 """
 
 import argparse
@@ -121,6 +125,94 @@ def cpu_baseline(w, min_seconds=10.0):
     }
 
 
+def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
+    """Forward + backward GB/s of each op pair (norm, activation) on every workload:
+    (B_fwd + B_bwd) / (t_fwd + t_bwd) with algorithmic bytes, per-launch durations
+    from HIP-graph replays (launch-bound small kernels would otherwise measure the
+    host), cold and warm.
+
+    Cold: enough tensor sets (at most 64) that each kernel's launches cycle over at
+    least `cold_bytes` of distinct memory, and at least the workload's blocks;
+    forwards run over the sets in order, backwards in reverse (the training order).
+    Warm: one set, relaunched (inputs partly resident in the 256 MB memory-side
+    cache)."""
+    out = {}
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    for name, w in inputs.WORKLOADS.items():
+        nb = algorithmic_bytes(w)
+        names = list(nb)
+        eps = float(np.float32(w.norm.eps))
+        T = lambda a: inputs.storage_to_torch(a, dev)
+        base = (T(w.norm_x()), T(w.norm_dz()), T(w.act_x()), T(w.act_dy()))
+        set_bytes = sum(nb.values())
+        nsets = max(w.blocks, 3, min(64, -(-cold_bytes // min(nb.values()))))
+        nfwd = {"msrms": lmbp.msrms_fwd, "msln": lmbp.msln_fwd}[w.norm.op]
+        nbwd = {"msrms": lmbp.msrms_bwd, "msln": lmbp.msln_bwd}[w.norm.op]
+        afwd = {"resilu2": lmbp.resilu2_fwd, "regelu2": lmbp.regelu2_fwd}[w.act.op]
+        abwd = {"resilu2": lmbp.resilu2_bwd, "regelu2": lmbp.regelu2_bwd}[w.act.op]
+
+        def make_set(k):
+            # Set k holds the block-0 tensors rotated by k * 4099 elements: same
+            # values and distribution, distinct memory.
+            x, dz, g, dy = (t if k == 0 else torch.roll(t.view(-1), k * 4099).view_as(t) for t in base)
+            st = {"x": x, "dz": dz, "g": g, "dy": dy, "z": torch.empty_like(x),
+                  "rstd": torch.empty(w.norm.rows, dtype=torch.float32, device=dev),
+                  "h": torch.empty_like(g), "dg": torch.empty_like(dy), "dx": torch.empty_like(dz),
+                  "codes": torch.empty(lmbp.codes_words(g.numel()), dtype=torch.int32, device=dev)}
+            return [lambda: nfwd(st["x"], eps, z=st["z"], rstd=st["rstd"]),
+                    lambda: afwd(st["g"], y=st["h"], codes=st["codes"]),
+                    lambda: abwd(st["dy"], st["codes"], dx=st["dg"]),
+                    lambda: nbwd(st["dz"], st["z"], st["rstd"], dx=st["dx"])]
+
+        sets = [make_set(k) for k in range(nsets)]
+        for ks in sets:
+            ks[0]()
+            ks[1]()
+        torch.cuda.synchronize()
+
+        def launch_us(i, order):
+            """Average duration of kernel i over `reps` launches cycling through `order`."""
+            seq = [order[j % len(order)] for j in range(max(reps, len(order)))]
+            side = torch.cuda.Stream()
+            side.wait_stream(torch.cuda.current_stream())
+            with torch.cuda.stream(side):
+                for k in seq:
+                    sets[k][i]()
+            torch.cuda.current_stream().wait_stream(side)
+            graph = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(graph):
+                for k in seq:
+                    sets[k][i]()
+            graph.replay()
+            a, b = mk(), mk()
+            a.record()
+            graph.replay()
+            graph.replay()
+            b.record()
+            torch.cuda.synchronize()
+            us = a.elapsed_time(b) * 1e3 / (2 * len(seq))
+            del graph
+            return us
+
+        fwd_order = list(range(nsets))
+        bwd_order = fwd_order[::-1]
+        cold = {n: launch_us(i, bwd_order if n.endswith("_bwd") else fwd_order) for i, n in enumerate(names)}
+        warm = {n: launch_us(i, [0]) for i, n in enumerate(names)}
+        rec = {"sets": nsets, "set_bytes": set_bytes}
+        for pair, (f, b) in (("norm", (names[0], names[3])), ("act", (names[1], names[2]))):
+            byt = nb[f] + nb[b]
+            gbs = byt / ((cold[f] + cold[b]) * 1e-6) / 1e9
+            rec[pair] = {"op": f[:-4], "fwd_us": round(cold[f], 2), "bwd_us": round(cold[b], 2),
+                         "bytes": byt, "GBps": round(gbs, 1), "pct_of_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
+                         "warm_GBps": round(byt / ((warm[f] + warm[b]) * 1e-6) / 1e9, 1)}
+        out[name] = rec
+        print(f"[bench] pairs {name}: norm {rec['norm']['GBps']} GB/s, act {rec['act']['GBps']} GB/s "
+              f"({nsets} sets)", file=sys.stderr, flush=True)
+        del sets, base
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -129,6 +221,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--swiglu", action="store_true",
                     help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
+    ap.add_argument("--pairs", action="store_true",
+                    help="also report forward+backward GB/s of each op pair on every workload")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the hot path is row- and element-local and runs "
@@ -311,6 +405,10 @@ def main():
         "inter_kernel_us_per_step": round(ms_step * 1e3 - sum(per_kernel_ms.values()) * 1e3, 2),
         "wall_s_timed": round(t_wall, 4),
     }
+    if args.pairs:
+        print("[bench] op pairs on every workload", file=sys.stderr, flush=True)
+        out["pairs"] = pair_report(torch, lmbp, inputs, dev)
+        out["pairs"]["copy_GBps"] = out["copy_reference"]["GBps"]
     if not args.no_cpu_baseline and not args.swiglu:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)

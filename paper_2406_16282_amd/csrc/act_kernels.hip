@@ -97,6 +97,41 @@ __device__ inline uint32_t seg_code(float x) {
   return b0 | (b1 << 1);
 }
 
+#ifndef LMBP_ACT_CARRY_CODES
+#define LMBP_ACT_CARRY_CODES 1  // vector-path codes through compare masks and carry-in adds
+#endif
+
+// Codes of E elements, element e in bits 2e (bit 0 of its code) and 2e + 1 (bit 1),
+// built without materialising any per-element bool: each compare leaves a lane
+// mask, bit 0's masks are combined with scalar xors, and each bit enters the word
+// as the carry input of an add of the word to itself (p = 2p + bit, last element
+// first). That is three compares and two adds per element, against about eight
+// vector operations for the select-and-shift form.
+__device__ inline uint32_t shift_in(uint32_t p, uint64_t lane_mask) {
+  uint32_t r;
+  uint64_t carry_out;
+  asm("v_addc_co_u32_e64 %0, %1, %2, %2, %3" : "=v"(r), "=s"(carry_out) : "v"(p), "s"(lane_mask));
+  return r;
+}
+
+template <class A, int E>
+__device__ inline uint32_t codes_of(const float (&f)[E]) {
+  uint32_t p = 0;
+#if LMBP_ACT_CARRY_CODES
+#pragma unroll
+  for (int e = E - 1; e >= 0; --e) {
+    const uint64_t m2 = __builtin_amdgcn_ballot_w64(f[e] > A::t2);
+    const uint64_t m0 = __builtin_amdgcn_ballot_w64(f[e] > A::t1) ^ m2 ^
+                        __builtin_amdgcn_ballot_w64(f[e] > A::t3);
+    p = shift_in(shift_in(p, m2), m0);
+  }
+#else
+#pragma unroll
+  for (int e = 0; e < E; ++e) p |= seg_code<A>(f[e]) << (2 * e);
+#endif
+  return p;
+}
+
 template <class A>
 __device__ inline float seg_slope(uint32_t c) {
   return (c & 2u) ? ((c & 1u) ? 1.0f : A::s2) : ((c & 1u) ? A::s1 : 0.0f);
@@ -200,13 +235,9 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void act_fwd_kernel(const void* x, 
     for (int j = 0; j < VPL; ++j) {
       float f[E], o[E];
       IO::unpack(in[j], f);
-      uint32_t p = 0;
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        o[e] = act_value<ACT, kPrecise>(f[e]);
-        p |= seg_code<A>(f[e]) << (2 * e);
-      }
-      part[j] = p;
+      for (int e = 0; e < E; ++e) o[e] = act_value<ACT, kPrecise>(f[e]);
+      part[j] = codes_of<A>(f);
       stg16<kActNtStore>(y, vbase + j * kWave + lane, IO::pack(o));
     }
 
@@ -302,14 +333,12 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void glu_fwd_kernel(const void* g, 
       float fg[E], fu[E], fs[E];
       IO::unpack(vg[j], fg);
       IO::unpack(vu[j], fu);
-      uint32_t p = 0;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         fs[e] = act_value<ACT, kPrecise>(fg[e]);
         fu[e] = fs[e] * fu[e];
-        p |= seg_code<A>(fg[e]) << (2 * e);
       }
-      part[j] = p;
+      part[j] = codes_of<A>(fg);
       stg16<kActNtStore>(s, vbase + j * kWave + lane, IO::pack(fs));
       stg16<kActNtStore>(h, vbase + j * kWave + lane, IO::pack(fu));
     }

@@ -11,11 +11,23 @@ namespace lmbp {
 // exp2 on the hardware unit (v_exp_f32); arguments here are never NaN.
 __device__ inline float hw_exp2(float v) { return __builtin_amdgcn_exp2f(v); }
 __device__ inline float hw_rcp(float v) { return __builtin_amdgcn_rcpf(v); }
+// max(x, 0) as one v_max_f32. The compiler's fmaxf first quiets a possible
+// signalling NaN with an extra max of x with itself (IEEE mode); inputs here are
+// finite, so that operation is pure overhead.
+__device__ inline float hw_relu(float x) {
+  float r;
+  asm("v_max_f32 %0, 0, %1" : "=v"(r) : "v"(x));
+  return r;
+}
+// min(t, hi) for t >= 0 as one v_med3_f32 (median of t, hi and 0), likewise
+// without the quieting operation of fminf.
+__device__ inline float hw_clamp_hi(float t, float hi) { return __builtin_amdgcn_fmed3f(t, hi, 0.0f); }
 
 // GELU(x) = x Phi(x). With t = |x| and Q(t) = 1 - Phi(t) = 2^E(t),
 // E(t) = -(log2 e / 2) t^2 + R(t), where R is the fitted polynomial of
 // gelu_poly.h (argument clamped to [0, T]). Phi(x) = Q(t) for x < 0 and 1 - Q(t)
-// otherwise.
+// otherwise, so GELU(x) = max(x, 0) - t Q(t) for either sign: one fused
+// multiply-add (rounded once) instead of a select, a subtraction and a product.
 //   PRECISE (fp32 storage): degree-12 R; the quadratic term is carried in two
 //   pieces and the exponent split into integer and fraction so that no rounding
 //   of the large exponent reaches the result (relative error below 1e-6).
@@ -35,7 +47,7 @@ __device__ inline float horner(const float (&c)[D], float v) {
 template <bool PRECISE>
 __device__ inline float gelu_f(float x) {
   const float t = __builtin_fabsf(x);
-  const float v = __builtin_fmaf(__builtin_fminf(t, LMBP_GELU_T), LMBP_GELU_2_OVER_T, -1.0f);
+  const float v = __builtin_fmaf(hw_clamp_hi(t, LMBP_GELU_T), LMBP_GELU_2_OVER_T, -1.0f);
   float q;
   if constexpr (PRECISE) {
     const float r = horner(kGeluR12, v);
@@ -49,8 +61,7 @@ __device__ inline float gelu_f(float x) {
     const float r = horner(kGeluR8, v);
     q = hw_exp2(__builtin_fmaf(t, t * -kLog2eHalfHi, r));
   }
-  const float phi = (x < 0.0f) ? q : 1.0f - q;
-  return x * phi;
+  return __builtin_fmaf(-t, q, hw_relu(x));
 }
 
 // SiLU(x) = x / (1 + 2^(-x log2 e)).

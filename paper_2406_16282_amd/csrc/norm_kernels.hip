@@ -268,30 +268,51 @@ __global__ __launch_bounds__(256) void norm_bwd_any(const void* dz, const void* 
 #ifndef LMBP_NORM_TARGET_VPL
 #define LMBP_NORM_TARGET_VPL 2  // preferred upper bound on vectors per thread
 #endif
+#ifndef LMBP_NORM_FWD_VPL
+#define LMBP_NORM_FWD_VPL LMBP_NORM_TARGET_VPL  // the forward kernel's target
+#endif
+#ifndef LMBP_NORM_BWD_VPL
+#define LMBP_NORM_BWD_VPL LMBP_NORM_TARGET_VPL  // the backward kernel's target
+#endif
 #ifndef LMBP_NORM_MAX_WPR
 #define LMBP_NORM_MAX_WPR 4  // widest row group (waves per row)
 #endif
+static_assert(LMBP_NORM_MAX_WPR == 1 || LMBP_NORM_MAX_WPR == 2 || LMBP_NORM_MAX_WPR == 4 ||
+                  LMBP_NORM_MAX_WPR == 8,
+              "waves per row must be 1, 2, 4 or 8");
 
 namespace {
 // Launch shape of the register-tile path: WPR waves per row and VPL 16-byte
 // vectors per thread, chosen from the row width in vectors (nv): the fewest waves
-// per row that keep VPL within the target (so registers stay low, occupancy high
-// and many rows are in flight per CU); rows wider than that use the widest group
-// with more vectors per thread, up to its capacity. Wider rows take the
-// block-per-row path.
+// per row that keep VPL within the direction's target (so registers stay low,
+// occupancy high and many rows are in flight per CU); rows wider than that use
+// the widest group with more vectors per thread, up to its capacity. Wider rows
+// take the block-per-row path. {0, 0} stands for that path.
 struct NormShape {
   int wpr, vpl;
 };
-constexpr int kVplSmall[] = {1, 2};
+constexpr int kVplSmall[] = {1, 2, 3, 4, 6, 8};
 constexpr int kVplWide[] = {1, 2, 3, 4, 6, 8, 12, 16};
 
-template <class IO>
-NormShape pick_shape(int64_t cols) {
-  const int64_t nv = cols / IO::kPerVec;
+constexpr bool in_list(int v, const int* list, int n) {
+  for (int i = 0; i < n; ++i)
+    if (list[i] == v) return true;
+  return false;
+}
+
+// Whether pick_shape can return (wpr, vpl) for the given target; only those
+// shapes are instantiated.
+constexpr bool reachable(int wpr, int vpl, int target) {
+  if (wpr > LMBP_NORM_MAX_WPR) return false;
+  if (in_list(vpl, kVplSmall, 6) && vpl <= target) return true;
+  return wpr == LMBP_NORM_MAX_WPR && in_list(vpl, kVplWide, 8) && (wpr < 8 || vpl <= 8);
+}
+
+NormShape pick_shape(int64_t nv, int target) {
   for (int wpr = 1; wpr <= LMBP_NORM_MAX_WPR; wpr *= 2) {
-    if (int64_t(kWave) * wpr * LMBP_NORM_TARGET_VPL < nv) continue;
+    if (int64_t(kWave) * wpr * target < nv) continue;
     for (int v : kVplSmall)
-      if (int64_t(kWave) * wpr * v >= nv) return {wpr, v};
+      if (v <= target && int64_t(kWave) * wpr * v >= nv) return {wpr, v};
   }
   const int wpr = LMBP_NORM_MAX_WPR;
   for (int v : kVplWide) {
@@ -301,53 +322,62 @@ NormShape pick_shape(int64_t cols) {
   return {0, 0};
 }
 
-template <class IO, bool LN, int VPL, int WPR>
-hipError_t fwd_vec(int64_t rows, int cols, float eps, const void* x, void* z, float* rstd,
-                   hipStream_t s) {
-  constexpr int rpb = norm_block<WPR>() / (kWave * WPR);
-  const int64_t blocks = (rows + rpb - 1) / rpb;
-  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((norm_fwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(norm_block<WPR>()),
-                     0, s, x, z, rstd, rows, cols, eps);
-  return hipGetLastError();
+// Every shape the selection could produce for some knob setting, in one list; the
+// dispatchers below walk it at compile time and instantiate the reachable ones.
+constexpr NormShape kShapes[] = {
+    {1, 1}, {1, 2}, {1, 3}, {1, 4}, {1, 6}, {1, 8},
+    {2, 1}, {2, 2}, {2, 3}, {2, 4}, {2, 6}, {2, 8}, {2, 12}, {2, 16},
+    {4, 1}, {4, 2}, {4, 3}, {4, 4}, {4, 6}, {4, 8}, {4, 12}, {4, 16},
+    {8, 1}, {8, 2}, {8, 3}, {8, 4}, {8, 6}, {8, 8}};
+constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
+
+template <class IO, bool LN, int I>
+hipError_t fwd_dispatch(NormShape sh, int64_t rows, int cols, float eps, const void* x, void* z,
+                        float* rstd, hipStream_t s) {
+  if constexpr (I == kNumShapes) {
+    return hipErrorNotSupported;
+  } else {
+    constexpr int W = kShapes[I].wpr, V = kShapes[I].vpl;
+    if constexpr (reachable(W, V, LMBP_NORM_FWD_VPL)) {
+      if (sh.wpr == W && sh.vpl == V) {
+        constexpr int rpb = norm_block<W>() / (kWave * W);
+        const int64_t blocks = (rows + rpb - 1) / rpb;
+        if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((norm_fwd_vec<IO, LN, V, W>), dim3(unsigned(blocks)), dim3(norm_block<W>()),
+                           0, s, x, z, rstd, rows, cols, eps);
+        return hipGetLastError();
+      }
+    }
+    return fwd_dispatch<IO, LN, I + 1>(sh, rows, cols, eps, x, z, rstd, s);
+  }
 }
-template <class IO, bool LN, int VPL, int WPR>
-hipError_t bwd_vec(int64_t rows, int cols, const void* dz, const void* z, const float* rstd,
-                   void* dx, hipStream_t s) {
-  constexpr int rpb = norm_block<WPR>() / (kWave * WPR);
-  const int64_t blocks = (rows + rpb - 1) / rpb;
-  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  hipLaunchKernelGGL((norm_bwd_vec<IO, LN, VPL, WPR>), dim3(unsigned(blocks)), dim3(norm_block<WPR>()),
-                     0, s, dz, z, rstd, dx, rows, cols);
-  return hipGetLastError();
+
+template <class IO, bool LN, int I>
+hipError_t bwd_dispatch(NormShape sh, int64_t rows, int cols, const void* dz, const void* z,
+                        const float* rstd, void* dx, hipStream_t s) {
+  if constexpr (I == kNumShapes) {
+    return hipErrorNotSupported;
+  } else {
+    constexpr int W = kShapes[I].wpr, V = kShapes[I].vpl;
+    if constexpr (reachable(W, V, LMBP_NORM_BWD_VPL)) {
+      if (sh.wpr == W && sh.vpl == V) {
+        constexpr int rpb = norm_block<W>() / (kWave * W);
+        const int64_t blocks = (rows + rpb - 1) / rpb;
+        if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+        hipLaunchKernelGGL((norm_bwd_vec<IO, LN, V, W>), dim3(unsigned(blocks)), dim3(norm_block<W>()),
+                           0, s, dz, z, rstd, dx, rows, cols);
+        return hipGetLastError();
+      }
+    }
+    return bwd_dispatch<IO, LN, I + 1>(sh, rows, cols, dz, z, rstd, dx, s);
+  }
 }
 
 template <class IO, bool LN>
 hipError_t norm_fwd_t(int64_t rows, int64_t cols, float eps, const void* x, void* z, float* rstd,
                       bool vec_ok, hipStream_t s) {
-  const NormShape sh = vec_ok ? pick_shape<IO>(cols) : NormShape{0, 0};
-  const int c = int(cols);
-  switch (sh.wpr * 100 + sh.vpl) {
-    case 101: return fwd_vec<IO, LN, 1, 1>(rows, c, eps, x, z, rstd, s);
-    case 102: return fwd_vec<IO, LN, 2, 1>(rows, c, eps, x, z, rstd, s);
-    case 201: return fwd_vec<IO, LN, 1, 2>(rows, c, eps, x, z, rstd, s);
-    case 202: return fwd_vec<IO, LN, 2, 2>(rows, c, eps, x, z, rstd, s);
-    case 401: return fwd_vec<IO, LN, 1, 4>(rows, c, eps, x, z, rstd, s);
-    case 402: return fwd_vec<IO, LN, 2, 4>(rows, c, eps, x, z, rstd, s);
-    case 403: return fwd_vec<IO, LN, 3, 4>(rows, c, eps, x, z, rstd, s);
-    case 404: return fwd_vec<IO, LN, 4, 4>(rows, c, eps, x, z, rstd, s);
-    case 406: return fwd_vec<IO, LN, 6, 4>(rows, c, eps, x, z, rstd, s);
-    case 408: return fwd_vec<IO, LN, 8, 4>(rows, c, eps, x, z, rstd, s);
-    case 412: return fwd_vec<IO, LN, 12, 4>(rows, c, eps, x, z, rstd, s);
-    case 416: return fwd_vec<IO, LN, 16, 4>(rows, c, eps, x, z, rstd, s);
-    case 801: return fwd_vec<IO, LN, 1, 8>(rows, c, eps, x, z, rstd, s);
-    case 802: return fwd_vec<IO, LN, 2, 8>(rows, c, eps, x, z, rstd, s);
-    case 803: return fwd_vec<IO, LN, 3, 8>(rows, c, eps, x, z, rstd, s);
-    case 804: return fwd_vec<IO, LN, 4, 8>(rows, c, eps, x, z, rstd, s);
-    case 806: return fwd_vec<IO, LN, 6, 8>(rows, c, eps, x, z, rstd, s);
-    case 808: return fwd_vec<IO, LN, 8, 8>(rows, c, eps, x, z, rstd, s);
-    default: break;
-  }
+  const NormShape sh = vec_ok ? pick_shape(cols / IO::kPerVec, LMBP_NORM_FWD_VPL) : NormShape{0, 0};
+  if (sh.wpr != 0) return fwd_dispatch<IO, LN, 0>(sh, rows, int(cols), eps, x, z, rstd, s);
   if (rows > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((norm_fwd_any<IO, LN>), dim3(unsigned(rows)), dim3(256), 0, s, x, z, rstd, rows,
                      cols, eps);
@@ -357,29 +387,8 @@ hipError_t norm_fwd_t(int64_t rows, int64_t cols, float eps, const void* x, void
 template <class IO, bool LN>
 hipError_t norm_bwd_t(int64_t rows, int64_t cols, const void* dz, const void* z, const float* rstd,
                       void* dx, bool vec_ok, hipStream_t s) {
-  const NormShape sh = vec_ok ? pick_shape<IO>(cols) : NormShape{0, 0};
-  const int c = int(cols);
-  switch (sh.wpr * 100 + sh.vpl) {
-    case 101: return bwd_vec<IO, LN, 1, 1>(rows, c, dz, z, rstd, dx, s);
-    case 102: return bwd_vec<IO, LN, 2, 1>(rows, c, dz, z, rstd, dx, s);
-    case 201: return bwd_vec<IO, LN, 1, 2>(rows, c, dz, z, rstd, dx, s);
-    case 202: return bwd_vec<IO, LN, 2, 2>(rows, c, dz, z, rstd, dx, s);
-    case 401: return bwd_vec<IO, LN, 1, 4>(rows, c, dz, z, rstd, dx, s);
-    case 402: return bwd_vec<IO, LN, 2, 4>(rows, c, dz, z, rstd, dx, s);
-    case 403: return bwd_vec<IO, LN, 3, 4>(rows, c, dz, z, rstd, dx, s);
-    case 404: return bwd_vec<IO, LN, 4, 4>(rows, c, dz, z, rstd, dx, s);
-    case 406: return bwd_vec<IO, LN, 6, 4>(rows, c, dz, z, rstd, dx, s);
-    case 408: return bwd_vec<IO, LN, 8, 4>(rows, c, dz, z, rstd, dx, s);
-    case 412: return bwd_vec<IO, LN, 12, 4>(rows, c, dz, z, rstd, dx, s);
-    case 416: return bwd_vec<IO, LN, 16, 4>(rows, c, dz, z, rstd, dx, s);
-    case 801: return bwd_vec<IO, LN, 1, 8>(rows, c, dz, z, rstd, dx, s);
-    case 802: return bwd_vec<IO, LN, 2, 8>(rows, c, dz, z, rstd, dx, s);
-    case 803: return bwd_vec<IO, LN, 3, 8>(rows, c, dz, z, rstd, dx, s);
-    case 804: return bwd_vec<IO, LN, 4, 8>(rows, c, dz, z, rstd, dx, s);
-    case 806: return bwd_vec<IO, LN, 6, 8>(rows, c, dz, z, rstd, dx, s);
-    case 808: return bwd_vec<IO, LN, 8, 8>(rows, c, dz, z, rstd, dx, s);
-    default: break;
-  }
+  const NormShape sh = vec_ok ? pick_shape(cols / IO::kPerVec, LMBP_NORM_BWD_VPL) : NormShape{0, 0};
+  if (sh.wpr != 0) return bwd_dispatch<IO, LN, 0>(sh, rows, int(cols), dz, z, rstd, dx, s);
   if (rows > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((norm_bwd_any<IO, LN>), dim3(unsigned(rows)), dim3(256), 0, s, dz, z, rstd, dx,
                      rows, cols);
