@@ -1,7 +1,7 @@
 /*
  * lmbp.h - C ABI of the low-memory backpropagation kernels for AMD MI355X (gfx950).
  *
- * Eight operations from "Reducing Fine-Tuning Memory Overhead by Approximate and
+ * Operations from "Reducing Fine-Tuning Memory Overhead by Approximate and
  * Memory-Sharing Backpropagation" (Yang et al., ICML 2024):
  *
  *   regelu2_fwd / regelu2_bwd   ReGELU2  (Sec. 4.2; constants Appendix E)
@@ -10,6 +10,8 @@
  *   msrms_fwd   / msrms_bwd     MS-RMSNorm (Appendix G Alg. 3)
  *   reswiglu2_fwd / reswiglu2_bwd  ReSiLU2 fused with the SwiGLU product (LLaMA MLP)
  *   stepact_fwd / stepact_bwd      k-bit family members with runtime tables (ReGELU2-d, ...)
+ *   linear_act_fwd                 a linear layer whose output goes through ReGELU2 /
+ *                                  ReSiLU2, fused (the pre-activation stays on chip)
  *
  * Conventions shared by every call
  * --------------------------------
@@ -165,6 +167,34 @@ lmbp_status msrms_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps,
                       const void *x, void *z, float *rstd, void *stream);
 lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void *dz,
                       const void *z, const float *rstd, void *dx, void *stream);
+
+/* ------------------------------------------------------------------------
+ * Linear layer followed by ReGELU2 / ReSiLU2 (Sec. 4.2), forward, fused: the
+ * activation runs in the epilogue of the matrix product, so the pre-activation z,
+ * which the backward pass of ReGELU2 / ReSiLU2 does not need (it keeps only the
+ * codes), never has to be written out.
+ *
+ *   z = bf16( x W^T + b )        products accumulated in fp32, bias added in fp32,
+ *                                one rounding to bf16 (nearest even)
+ *   y = act(z), codes = 2-bit codes of z, exactly as regelu2_fwd / resilu2_fwd
+ *   compute them from a stored z (same bytes).
+ *
+ *   dt     : LMBP_BF16 only (LMBP_EDTYPE otherwise).
+ *   act    : LMBP_ACT_GELU (ReGELU2) or LMBP_ACT_SILU (ReSiLU2).
+ *   m,n,k  : x is m x k, w is n x k (the weight of a linear layer, row-major), y and
+ *            z are m x n. n must be a multiple of 16 (each row of codes fills whole
+ *            words) and k a multiple of 8; m, n >= 0, k >= 0 (k == 0 gives z = b).
+ *   x, w, y, z : 16-byte aligned.
+ *   bias   : n bf16 values, or NULL for none.
+ *   codes  : lmbp_codes_bytes(m * n) bytes, codes of the flattened m x n output.
+ *   z      : NULL (not stored) or m x n bf16.
+ * y, codes and z must not overlap each other or any input. The backward pass is
+ * regelu2_bwd / resilu2_bwd on the codes followed by the two products of a linear
+ * layer's backward.
+ * ------------------------------------------------------------------------ */
+lmbp_status linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
+                           const void *x, const void *w, const void *bias, void *y,
+                           uint32_t *codes, void *z, void *stream);
 
 /* ------------------------------------------------------------------------
  * Measurement utility (not part of the method): copies `bytes` bytes from src

@@ -17,6 +17,8 @@ What it computes, each function citing the passage it follows:
 * ``norms``: MS-LN and MS-RMSNorm (Sec. 5.2 Alg. 1; Appendix G Alg. 2 and Alg. 3):
   forward ``z = H x / sigma`` saving ``z`` and ``1/sigma``; backward
   ``dx = sigma^-1 (H - p^-1 z z^T) dz`` from the saved output alone.
+* ``linear``: a linear layer z = x W^T + b whose output, rounded once to bf16, feeds
+  ReGELU2 / ReSiLU2 (the fused forward of the MLP's first projection).
 * ``dtypes``: decoding of fp32 / bf16 storage to fp64 and correct round-to-nearest-even
   encoding of fp64 results back to storage.
 
@@ -35,6 +37,7 @@ from .activations import (
 )
 from .norms import msln_fwd, msln_bwd, msrms_fwd, msrms_bwd
 from . import variants
+from .linear import linear, linear_act_fwd
 
 __all__ = [
     "decode", "encode", "round_to_dtype", "DTYPES",
@@ -44,4 +47,5 @@ __all__ = [
     "regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd",
     "reswiglu2_fwd", "reswiglu2_bwd",
     "msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd", "variants",
+    "linear", "linear_act_fwd",
 ]

@@ -1,0 +1,37 @@
+"""A linear layer whose output feeds ReGELU2 / ReSiLU2 (Sec. 4.2).
+
+Test infrastructure only (see the package docstring).
+
+The activation's input is the output z = x W^T + b of the preceding linear layer
+(the MLP's first projection in ViT and LLaMA blocks). The fused GPU operation rounds
+z once to bf16 and applies the activation to the rounded value, so that its y and
+codes are those the stand-alone activation would produce from a stored bf16 z. The
+oracle writes that composition out: the exact product in float64, the one rounding,
+then the activation oracle of ``activations``.
+"""
+
+import numpy as np
+
+from .activations import regelu2_fwd, resilu2_fwd
+from .dtypes import decode, encode
+
+
+def linear(x, w, b=None):
+    """z = x W^T + b in float64 (x [m, k], w [n, k] as an nn.Linear weight, b [n])."""
+    x = np.asarray(x, dtype=np.float64)
+    w = np.asarray(w, dtype=np.float64)
+    z = x @ w.T
+    if b is not None:
+        z = z + np.asarray(b, dtype=np.float64)[None, :]
+    return z
+
+
+def linear_act_fwd(x_bf16, w_bf16, b_bf16, act):
+    """The fused forward on bf16 storage: returns (z exact, z stored as bf16 bits,
+    y in float64 (the activation of the stored z), packed codes of the stored z)."""
+    z = linear(decode(x_bf16, "bf16"), decode(w_bf16, "bf16"),
+               None if b_bf16 is None else decode(b_bf16, "bf16"))
+    z_s = encode(z, "bf16")
+    fwd = {"gelu": regelu2_fwd, "silu": resilu2_fwd}[act]
+    y, codes = fwd(decode(z_s, "bf16"))
+    return z, z_s, y, codes

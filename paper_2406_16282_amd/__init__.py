@@ -3,8 +3,10 @@ Memory-Sharing Backpropagation (Yang et al., ICML 2024).
 
 ReGELU2 / ReSiLU2 keep the exact activation in the forward pass and save only a
 2-bit segment code per element for a step-function derivative in the backward
-pass (Sec. 4.2); ReSiLU2 also comes fused with the SwiGLU product of the LLaMA MLP. MS-LN / MS-RMSNorm, with the affine merged into the next linear
-layer, save only their output and one fp32 statistic per row (Sec. 5.2).
+pass (Sec. 4.2); ReSiLU2 also comes fused with the SwiGLU product of the LLaMA
+MLP, and both come fused into the epilogue of the preceding linear layer's matrix
+product (bf16 MFMA). MS-LN / MS-RMSNorm, with the affine merged into the next
+linear layer, save only their output and one fp32 statistic per row (Sec. 5.2).
 
 The kernels live in liblmbp.so (C ABI in include/lmbp.h); ``binding`` marshals
 torch tensors into it. The library is loaded on first use.
@@ -16,6 +18,7 @@ from .binding import (  # noqa: F401
     codes_words,
     copy_bytes,
     lib,
+    linear_act_fwd,
     msln_bwd,
     msln_fwd,
     msrms_bwd,

@@ -8,6 +8,7 @@ built, the first call raises.
 """
 
 import ctypes
+import math
 import os
 
 import torch
@@ -22,6 +23,7 @@ ACT_OPS = ("regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd")
 NORM_OPS = ("msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd")
 GLU_OPS = ("reswiglu2_fwd", "reswiglu2_bwd")
 STEP_OPS = ("stepact_fwd", "stepact_bwd")
+LINEAR_OPS = ("linear_act_fwd",)
 ACT_GELU, ACT_SILU = 0, 1
 
 
@@ -74,6 +76,8 @@ def lib():
     L.stepact_fwd.restype = i32
     L.stepact_bwd.argtypes = [i32, dp, i32, i64, vp, vp, vp, vp]
     L.stepact_bwd.restype = i32
+    L.linear_act_fwd.argtypes = [i32, i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
+    L.linear_act_fwd.restype = i32
     L.lmbp_copy.argtypes = [vp, vp, i64, vp]
     L.lmbp_copy.restype = i32
     _lib = L
@@ -334,3 +338,45 @@ def copy_bytes(src, dst, stream=None):
         raise ValueError("src and dst must have the same byte size")
     _check("lmbp_copy", lib().lmbp_copy(_ptr(src), _ptr(dst), nbytes, _stream(src, stream)))
     return dst
+
+
+def linear_act_fwd(x, w, bias=None, act="gelu", y=None, codes=None, z=None, store_z=False,
+                   stream=None):
+    """Fused linear layer + ReGELU2 / ReSiLU2 forward (bf16): z = bf16(x W^T + b),
+    y = act(z), codes of z. x is [..., k], w is [n, k] (nn.Linear weight), bias [n] or
+    None. Returns (y, codes) or, with store_z (or a z tensor given), (y, codes, z)."""
+    if act not in ("gelu", "silu"):
+        raise ValueError("act must be 'gelu' or 'silu'")
+    _dev(x, "x")
+    _dev(w, "w")
+    if x.dtype != torch.bfloat16 or w.dtype != torch.bfloat16:
+        raise TypeError("linear_act_fwd takes bfloat16 x and w")
+    if w.dim() != 2 or x.shape[-1] != w.shape[1]:
+        raise ValueError("x must be [..., k] and w [n, k]")
+    n, k = w.shape
+    m = math.prod(x.shape[:-1])
+    out_shape = (*x.shape[:-1], n)
+    if bias is not None:
+        _dev(bias, "bias")
+        if bias.dtype != torch.bfloat16 or bias.numel() != n:
+            raise ValueError("bias must be a bfloat16 tensor of n elements")
+    if y is None:
+        y = torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
+    else:
+        _dev(y, "y")
+        if y.dtype != torch.bfloat16 or y.numel() != m * n:
+            raise ValueError("y must be a bfloat16 tensor of m * n elements")
+    if z is None and store_z:
+        z = torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
+    elif z is not None:
+        _dev(z, "z")
+        if z.dtype != torch.bfloat16 or z.numel() != m * n:
+            raise ValueError("z must be a bfloat16 tensor of m * n elements")
+    codes = _codes_out(m * n, x.device, codes)
+    L = lib()
+    _check("linear_act_fwd", L.linear_act_fwd(ACT_GELU if act == "gelu" else ACT_SILU, BF16, m, n, k,
+                                              _ptr(x), _ptr(w),
+                                              _ptr(bias) if bias is not None else None,
+                                              _ptr(y), _ptr(codes),
+                                              _ptr(z) if z is not None else None, _stream(x, stream)))
+    return (y, codes, z) if z is not None else (y, codes)

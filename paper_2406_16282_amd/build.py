@@ -16,7 +16,8 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(HERE, "liblmbp.so")
-SOURCES = ("lmbp_api.hip", "act_kernels.hip", "norm_kernels.hip", "stepact_kernels.hip")
+SOURCES = ("lmbp_api.hip", "act_kernels.hip", "norm_kernels.hip", "stepact_kernels.hip",
+           "linear_kernels.hip")
 ARCH = "gfx950"
 
 COMMON_FLAGS = [

@@ -236,6 +236,39 @@ lmbp_status norm_bwd(bool ln, lmbp_dtype dt, int64_t rows, int64_t cols, const v
                                         static_cast<hipStream_t>(stream)));
 }
 
+lmbp_status linear_act_fwd_impl(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
+                                const void* x, const void* w, const void* bias, void* y,
+                                uint32_t* codes, void* z, void* stream) {
+  if (!known_dtype(dt)) return LMBP_EDTYPE;
+  if (dt != LMBP_BF16) return LMBP_EDTYPE;
+  if (act != LMBP_ACT_GELU && act != LMBP_ACT_SILU) return LMBP_EINVAL;
+  const int64_t lim = int64_t(1) << 31;
+  if (m < 0 || n < 0 || k < 0 || m >= lim || n >= lim || k >= lim) return LMBP_EINVAL;
+  if (n % 16 != 0 || k % 8 != 0) return LMBP_EINVAL;
+  if (m == 0 || n == 0) return LMBP_OK;
+  if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (!y || !codes || (k > 0 && (!x || !w))) return LMBP_EINVAL;
+  if ((x && !aligned(x, 16)) || (w && !aligned(w, 16)) || !aligned(y, 16) || (z && !aligned(z, 16)) ||
+      !aligned(codes, 4) || (bias && !aligned(bias, 2)))
+    return LMBP_EINVAL;
+  const uint64_t mn = uint64_t(m) * uint64_t(n);
+  const Span sy = span(y, mn * 2), sc = span(codes, lmbp_codes_bytes(int64_t(mn)));
+  const Span sz = span(z, z ? mn * 2 : 0);
+  const Span ins[3] = {span(x, x ? uint64_t(m) * uint64_t(k) * 2 : 0),
+                       span(w, w ? uint64_t(n) * uint64_t(k) * 2 : 0),
+                       span(bias, bias ? uint64_t(n) * 2 : 0)};
+  const Span outs[3] = {sy, sc, sz};
+  for (int i = 0; i < 3; ++i) {
+    for (int j = i + 1; j < 3; ++j)
+      if (overlaps(outs[i], outs[j])) return LMBP_EOVERLAP;
+    for (const Span& in : ins)
+      if (overlaps(outs[i], in)) return LMBP_EOVERLAP;
+  }
+  return from_hip(lmbp::launch_linear_act_fwd(act == LMBP_ACT_GELU ? lmbp::kGelu : lmbp::kSilu, m,
+                                              n, k, x, w, bias, y, codes, z,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -308,6 +341,12 @@ lmbp_status msrms_fwd(lmbp_dtype dt, int64_t rows, int64_t cols, float eps, cons
 lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void* dz, const void* z,
                       const float* rstd, void* dx, void* stream) {
   return norm_bwd(false, dt, rows, cols, dz, z, rstd, dx, stream);
+}
+
+lmbp_status linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
+                           const void* x, const void* w, const void* bias, void* y,
+                           uint32_t* codes, void* z, void* stream) {
+  return linear_act_fwd_impl(act, dt, m, n, k, x, w, bias, y, codes, z, stream);
 }
 
 lmbp_status lmbp_copy(const void* src, void* dst, int64_t bytes, void* stream) {

@@ -40,6 +40,12 @@ hipError_t launch_stepact_fwd(int act, int bits, bool bf16, int64_t n, const voi
 hipError_t launch_stepact_bwd(int bits, bool bf16, int64_t n, const void* dy, const uint32_t* codes,
                               void* dx, bool vec_ok, const StepTable& tab, hipStream_t s);
 
+// z = bf16(x W^T + bias) (bf16 operands, fp32 accumulation); y = act(z), codes of z;
+// z stored when non-null. N % 16 == 0, K % 8 == 0, x/w/y/z 16-byte aligned.
+hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const void* x,
+                                 const void* w, const void* bias, void* y, uint32_t* codes,
+                                 void* z, hipStream_t s);
+
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
 
 }  // namespace lmbp

@@ -23,6 +23,7 @@ import numpy as np
 
 SEED = 0
 NORM_X, NORM_DZ, ACT_X, ACT_DY, ACT_U = 0, 1, 2, 3, 4
+LIN_X, LIN_W, LIN_B = 5, 6, 7
 
 
 def rng(seed, block, tensor_id):
@@ -52,6 +53,15 @@ def to_storage(a64, dtype):
 def normal(shape, std, dtype, seed=SEED, block=0, tensor_id=0, mean=0.0):
     g = rng(seed, block, tensor_id)
     return to_storage(mean + std * g.standard_normal(size=shape), dtype)
+
+
+def dyadic(shape, exponent, seed=SEED, block=0, tensor_id=0, span=8):
+    """Integers in [-span, span] times 2^exponent, as bf16 patterns. Products and sums
+    of such values stay exactly representable in fp32 for moderate sizes, so any
+    summation order gives the exact result."""
+    g = rng(seed, block, tensor_id)
+    v = g.integers(-span, span + 1, size=shape).astype(np.float64) * 2.0 ** exponent
+    return to_storage(v, "bf16")
 
 
 def outlier_mixture(shape, dtype, seed=SEED, block=0, tensor_id=0,

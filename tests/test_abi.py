@@ -125,6 +125,30 @@ def test_swiglu_errors(L):
     assert b(B.BF16, 16, dh, u, s, dg + 4, dg, du, None) == B.EOVERLAP
 
 
+def test_linear_act_errors(L):
+    f = L.linear_act_fwd
+    G = B.ACT_GELU
+    # m = 4, n = 32, k = 16: x 128 B, w 1024 B, bias 64 B, y / z 256 B, codes 32 B
+    x, w, bias, y, c, z = P, P + 4096, P + 8192, P + 12288, P + 16384, P + 20480
+    assert f(G, B.FP32, 4, 32, 16, x, w, bias, y, c, z, None) == B.EDTYPE
+    assert f(G, 7, 4, 32, 16, x, w, bias, y, c, z, None) == B.EDTYPE
+    assert f(9, B.BF16, 4, 32, 16, x, w, bias, y, c, z, None) == B.EINVAL
+    assert f(G, B.BF16, -1, 32, 16, x, w, bias, y, c, z, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 24, 16, x, w, bias, y, c, z, None) == B.EINVAL     # n % 16
+    assert f(G, B.BF16, 4, 32, 12, x, w, bias, y, c, z, None) == B.EINVAL     # k % 8
+    assert f(G, B.BF16, 0, 32, 16, x, w, bias, y, c, z, None) == B.OK         # empty
+    assert f(G, B.BF16, 4, 0, 16, x, w, bias, y, c, z, None) == B.OK
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias, None, c, z, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 32, 16, None, w, bias, y, c, z, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 32, 16, x + 8, w, bias, y, c, z, None) == B.EINVAL   # 16-byte alignment
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias, y, c, z + 2, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias + 1, y, c, z, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias, y, c, y + 16, None) == B.EOVERLAP  # z overlaps y
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias, y, x + 64, z, None) == B.EOVERLAP  # codes on x
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias, w, c, z, None) == B.EOVERLAP       # y on w
+    assert f(G, B.BF16, 4, 32, 16, x, w, bias, y, c, bias - 16, None) == B.EOVERLAP
+
+
 def test_copy_errors(L):
     assert L.lmbp_copy(P, P + 4096, -1, None) == B.EINVAL
     assert L.lmbp_copy(P, P + 4096, 0, None) == B.OK

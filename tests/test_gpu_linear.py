@@ -1,0 +1,156 @@
+"""GPU parity of the fused linear layer + ReGELU2 / ReSiLU2 forward against the CPU
+oracle, through the C ABI.
+
+Exact cases: dyadic bf16 inputs (small integers times powers of two) keep every
+product and partial sum exactly representable in fp32, so any accumulation order
+gives the exact z; the stored z must equal the oracle's correctly rounded z bit for
+bit, the codes bit for bit, and y the activation oracle's value under the activation
+rules. Realistic cases (normal inputs): fp32 accumulation error is far below a bf16
+step for all but near-zero sums, so the stored z is nearly always the oracle's
+rounding itself, and always within a bound derived from the summation; every code must lie in
+the range of codes admissible under that bound (and nearly always equal the oracle's);
+y must meet the mixed rule."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2406_16282_amd as lmbp
+from paper_2406_16282_amd import inputs
+from compare import assert_codes_equal, assert_mixed, assert_rel, bf16_ulp_distance
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+THRESH = {"gelu": oracle.GELU_C, "silu": oracle.SILU_C}
+
+
+def T(a):
+    return inputs.storage_to_torch(a, DEV)
+
+
+def H(t):
+    return inputs.torch_to_storage(t)
+
+
+def run(x, w, b, act, store_z=True):
+    out = lmbp.linear_act_fwd(T(x), T(w), None if b is None else T(b), act=act, store_z=store_z)
+    torch.cuda.synchronize()
+    return tuple(H(t) for t in out)
+
+
+def check_exact(m, n, k, act, bias, label):
+    print(f"[linear] exact {label}: m={m} n={n} k={k} act={act} bias={bias}", flush=True)
+    x = inputs.dyadic((m, k), -3, tensor_id=inputs.LIN_X, block=m + n + k)
+    w = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_W, block=m + n + k)
+    b = inputs.dyadic((n,), -7, tensor_id=inputs.LIN_B, block=m + n + k) if bias else None
+    _, z_s, y_o, c_o = oracle.linear_act_fwd(x, w, b, act)
+    y, codes, z = run(x, w, b, act)
+    assert np.array_equal(z, z_s), f"{label}: stored z differs from the exact rounding"
+    assert_codes_equal(codes, c_o, f"{label} codes")
+    y64 = oracle.decode(y, "bf16")
+    assert_rel(y64, y_o, 1e-2, f"{label} y (strict)")
+    m_ = np.abs(y_o) >= 2.0 ** -60
+    d = bf16_ulp_distance(y, y_o)[m_]
+    assert d.max() <= 1, f"{label}: y more than one bf16 step from the oracle"
+    if d.size >= 1000:
+        assert np.mean(d == 0) >= 0.99, f"{label}: y correctly rounded for too few elements"
+
+
+EXACT_SHAPES = [
+    (128, 128, 64),      # one tile, one K step
+    (64, 48, 8),         # partial tile in m and n, shortest K
+    (200, 272, 200),     # several tiles, ragged m, n and K (K not a multiple of 64)
+    (300, 384, 1024),    # many K steps
+    (1, 16, 24),         # one row, one code-word column group
+]
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+@pytest.mark.parametrize("m,n,k", EXACT_SHAPES)
+def test_exact(m, n, k, act):
+    check_exact(m, n, k, act, bias=True, label=f"{m}x{n}x{k}")
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_exact_no_bias(act):
+    check_exact(96, 160, 136, act, bias=False, label="no bias")
+
+
+def test_k_zero_gives_bias():
+    """k = 0: z is the bias broadcast over the rows."""
+    m, n = 5, 32
+    b = inputs.normal((n,), 3.0, "bf16", tensor_id=inputs.LIN_B)
+    x = torch.empty((m, 0), dtype=torch.bfloat16, device=DEV)
+    w = torch.empty((n, 0), dtype=torch.bfloat16, device=DEV)
+    y, codes, z = lmbp.linear_act_fwd(x, w, T(b), act="gelu", store_z=True)
+    torch.cuda.synchronize()
+    assert np.array_equal(H(z), np.broadcast_to(b, (m, n)))
+    y_o, c_o = oracle.regelu2_fwd(oracle.decode(np.broadcast_to(b, (m, n)).copy(), "bf16"))
+    assert_codes_equal(H(codes), c_o, "k=0 codes")
+    assert_rel(oracle.decode(H(y), "bf16"), y_o, 1e-2, "k=0 y")
+
+
+def check_realistic(x, w, b, act, label, rows=None):
+    """Compare on `rows` (all rows when None) of the GPU result.
+
+    Bound on the stored z: the fp32 sum of k products and a bias, in any order, is
+    within gamma * S of the exact value, gamma = (k + 1) 2^-24 and S = sum |x_t w_t| + |b|
+    (products of two bf16 values are exact in fp32); one rounding to bf16 adds at most
+    2^-8 of the magnitude. Codes are monotone in z, so the code of any z in that
+    interval lies between the codes of its ends."""
+    print(f"[linear] realistic {label}: x={x.shape} w={w.shape} act={act}", flush=True)
+    y, codes, z = run(x, w, b, act)
+    m, n, k = x.shape[0], w.shape[0], x.shape[1]
+    rows = np.arange(m) if rows is None else rows
+    z_o, z_s, y_o, c_o = oracle.linear_act_fwd(x[rows], w, b, act)
+    S = oracle.linear(np.abs(oracle.decode(x[rows], "bf16")), np.abs(oracle.decode(w, "bf16")),
+                      None if b is None else np.abs(oracle.decode(b, "bf16")))
+    acc = (k + 1) * 2.0 ** -24 * S
+    bound = acc + 2.0 ** -8 * (np.abs(z_o) + acc)
+    zg = z.reshape(m, n)[rows]
+    err = np.abs(oracle.decode(zg, "bf16") - z_o)
+    assert np.all(err <= bound), f"{label}: stored z outside the accumulation + rounding bound " \
+                                 f"(worst err/bound {np.max(err / bound):.3g})"
+    exact = zg == z_s
+    assert np.mean(exact) >= 0.99, f"{label}: stored z is the correct rounding for too few elements"
+    got = oracle.unpack_codes(codes, m * n).reshape(m, n)[rows]
+    lo = oracle.segment_code(z_o - bound, THRESH[act])
+    hi = oracle.segment_code(z_o + bound, THRESH[act])
+    assert np.all((lo <= got) & (got <= hi)), f"{label}: a code outside the admissible range"
+    ref = oracle.unpack_codes(c_o, len(rows) * n).reshape(len(rows), n)
+    assert np.mean(got == ref) >= 0.999, f"{label}: codes equal the oracle's for too few elements"
+    assert_mixed(oracle.decode(y.reshape(m, n)[rows], "bf16"), y_o, 1e-2, f"{label} y")
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_realistic_vit_mlp(act):
+    """ViT-B MLP first projection, 300 tokens: x [300, 768], W [3072, 768]."""
+    x = inputs.normal((300, 768), 1.0, "bf16", tensor_id=inputs.LIN_X)
+    w = inputs.normal((3072, 768), 768 ** -0.5, "bf16", tensor_id=inputs.LIN_W)
+    b = inputs.normal((3072,), 0.1, "bf16", tensor_id=inputs.LIN_B)
+    check_realistic(x, w, b, act, "vit fc1")
+
+
+def test_full_size_llama_gate_sampled():
+    """LLaMA-7B gate projection at full size, x [8192, 4096], W [11008, 4096], no bias;
+    32 sampled rows (including the first and last) compared with the oracle."""
+    x = inputs.normal((8192, 4096), 1.0, "bf16", tensor_id=inputs.LIN_X)
+    w = inputs.normal((11008, 4096), 4096 ** -0.5 * 2.0, "bf16", tensor_id=inputs.LIN_W)
+    rows = np.unique(np.concatenate([[0, 8191], np.random.default_rng(7).integers(0, 8192, 30)]))
+    check_realistic(x, w, None, "silu", "llama gate", rows=rows)
+
+
+def test_store_z_does_not_change_outputs_and_matches_the_activation_op():
+    """Without z the outputs are the same bytes; with z they equal the stand-alone
+    activation kernel applied to that z (the documented contract)."""
+    x = inputs.normal((257, 512), 1.0, "bf16", tensor_id=inputs.LIN_X)
+    w = inputs.normal((640, 512), 512 ** -0.5 * 3.0, "bf16", tensor_id=inputs.LIN_W)
+    b = inputs.normal((640,), 0.5, "bf16", tensor_id=inputs.LIN_B)
+    for act, op in (("gelu", lmbp.regelu2_fwd), ("silu", lmbp.resilu2_fwd)):
+        y1, c1, z1 = run(x, w, b, act, store_z=True)
+        y2, c2 = run(x, w, b, act, store_z=False)
+        assert np.array_equal(y1, y2) and np.array_equal(c1, c2)
+        y3, c3 = op(T(z1))
+        torch.cuda.synchronize()
+        assert np.array_equal(H(y3), y1) and np.array_equal(H(c3), c1)
