@@ -17,7 +17,10 @@ event-timed loop that launches each kernel back to back over rotating tensor
 sets; the dominant kernel's figure feeds the roofline entry.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--swiglu] [--pairs]
+                      [--linear]
 
+--linear adds the fused linear-layer + activation forward (TFLOP/s, against the
+unfused library GEMM + activation kernel) on the ViT-B and LLaMA-7B MLP shapes.
 --pairs adds, for every workload (ViT-B fp32, ViT-B batch 64 bf16 x 12 blocks,
 LLaMA-7B and LLaMA-13B shapes), the forward + backward GB/s of the norm pair and
 of the activation pair, cold and warm.
@@ -40,6 +43,8 @@ HBM_PEAK_GBS = 8000.0            # MI355X HBM3E, AMD published peak
 WORKLOAD = "llama7b_swiglu_bf16"
 METRIC = "fwd+bwd HBM GB/s (% of peak) for ReGELU2/ReSiLU2/MS-LN; saved bytes/elt"
 KERNEL_SOURCES = ("paper_2406_16282_amd/csrc/act_kernels.hip",
+                  "paper_2406_16282_amd/csrc/act_codes.hpp",
+                  "paper_2406_16282_amd/csrc/act_math.hpp",
                   "paper_2406_16282_amd/csrc/norm_kernels.hip",
                   "paper_2406_16282_amd/csrc/lmbp_device.hpp",
                   "paper_2406_16282_amd/csrc/gelu_poly.h")
@@ -213,6 +218,77 @@ def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
     return out
 
 
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, AMD published
+
+LINEAR_SHAPES = {
+    # name: (m, n, k, act, bias) -- the MLP's first projection feeding the activation
+    "vit_b_bs64_fc1_bf16": (64 * 197, 3072, 768, "gelu", True),
+    "llama7b_gate_bf16": (4 * 2048, 11008, 4096, "silu", False),
+}
+
+
+def linear_report(torch, lmbp, inputs, dev, reps):
+    """Fused linear + ReGELU2 / ReSiLU2 forward against the unfused sequence (library
+    GEMM through torch, i.e. hipBLASLt, writing z, then the activation kernel reading
+    it), on the ViT-B and LLaMA-7B MLP shapes. Durations: HIP events around `reps`
+    back-to-back launches on the current stream."""
+    out = {}
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+
+    def timed(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        a, b = mk(), mk()
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps
+
+    for name, (m, n, k, act, has_bias) in LINEAR_SHAPES.items():
+        T = lambda a: inputs.storage_to_torch(a, dev)
+        x = T(inputs.normal((m, k), 1.0, "bf16", tensor_id=inputs.LIN_X))
+        w = T(inputs.normal((n, k), k ** -0.5 * 2.0, "bf16", tensor_id=inputs.LIN_W))
+        b = T(inputs.normal((n,), 0.1, "bf16", tensor_id=inputs.LIN_B)) if has_bias else None
+        y = torch.empty((m, n), dtype=torch.bfloat16, device=dev)
+        z = torch.empty((m, n), dtype=torch.bfloat16, device=dev)
+        codes = torch.empty(lmbp.codes_words(m * n), dtype=torch.int32, device=dev)
+        afwd = lmbp.regelu2_fwd if act == "gelu" else lmbp.resilu2_fwd
+        wt = w.t()
+
+        def gemm():
+            if b is None:
+                torch.matmul(x, wt, out=z)
+            else:
+                torch.addmm(b, x, wt, out=z)
+
+        t_fused = timed(lambda: lmbp.linear_act_fwd(x, w, b, act=act, y=y, codes=codes))
+        t_gemm = timed(gemm)
+        t_act = timed(lambda: afwd(z, y=y, codes=codes))
+        t_unfused = timed(lambda: (gemm(), afwd(z, y=y, codes=codes)))
+        flops = 2.0 * m * n * k
+        tf = flops / (t_fused * 1e-6) / 1e12
+        out[name] = {
+            "m": m, "n": n, "k": k, "act": act, "bias": has_bias,
+            "fused_us": round(t_fused, 1), "fused_TFLOPs": round(tf, 1),
+            "unfused_us": round(t_unfused, 1), "library_gemm_us": round(t_gemm, 1),
+            "act_kernel_us": round(t_act, 1),
+            "library_gemm_TFLOPs": round(flops / (t_gemm * 1e-6) / 1e12, 1),
+            "speedup_vs_unfused": round(t_unfused / t_fused, 3),
+            "hbm_bytes_saved": 2 * 2 * m * n,   # z written by the GEMM and read by the activation
+            "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+        }
+        print(f"[bench] linear {name}: fused {t_fused:.1f} us ({tf:.0f} TFLOP/s), unfused "
+              f"{t_unfused:.1f} us (library GEMM {t_gemm:.1f} + activation {t_act:.1f})",
+              file=sys.stderr, flush=True)
+        del x, w, b, y, z, codes
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -223,6 +299,9 @@ def main():
                     help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
     ap.add_argument("--pairs", action="store_true",
                     help="also report forward+backward GB/s of each op pair on every workload")
+    ap.add_argument("--linear", action="store_true",
+                    help="also report the fused linear + activation forward against the unfused "
+                         "library GEMM + activation kernel")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the hot path is row- and element-local and runs "
@@ -409,6 +488,9 @@ def main():
         print("[bench] op pairs on every workload", file=sys.stderr, flush=True)
         out["pairs"] = pair_report(torch, lmbp, inputs, dev)
         out["pairs"]["copy_GBps"] = out["copy_reference"]["GBps"]
+    if args.linear:
+        print("[bench] fused linear + activation", file=sys.stderr, flush=True)
+        out["linear"] = linear_report(torch, lmbp, inputs, dev, reps=max(10, min(args.steps, 50)))
     if not args.no_cpu_baseline and not args.swiglu:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w)

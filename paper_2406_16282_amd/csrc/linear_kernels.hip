@@ -9,14 +9,18 @@
 // the caller asks for it: ReGELU2 / ReSiLU2 keep only the codes for the backward
 // pass, so the pre-activation never has to reach HBM.
 //
-// Tiling: a 256-thread block computes a 128 x 128 tile of z, each of its four waves a
-// 64 x 64 quarter as 2 x 2 MFMA tiles of 32 x 32. K advances in steps of 64 through
-// two LDS buffers per operand; the global loads of the next step are in flight while
-// the MFMAs of the current one run. LDS rows are padded to 144 bytes so that the
-// 16-byte operand reads of 32 consecutive rows fall on distinct banks. Lane layout of
-// the MFMA (checked on the hardware): lane l supplies row l % 32 of A and column l % 32
-// of B at k = 8 (l / 32) .. + 7, and holds result rows 8 (r / 4) + 4 (l / 32) + r % 4
-// of column l % 32 in accumulator register r.
+// Tiling (defaults; measured best of the shapes tried on the LLaMA-7B gate and ViT-B
+// MLP projections): a 512-thread block computes a 256 x 256 tile of z, its eight waves
+// (4 along the rows, 2 along the columns) a 64 x 128 part each as 2 x 4 MFMA tiles of
+// 32 x 32, accumulators in registers. K advances in steps of 64 through two LDS
+// buffers per operand; global loads run two steps ahead of the MFMAs (two register
+// stages), as raw buffer loads whose range ends at the tile's last valid row, so
+// ragged tiles read zeros without branches. LDS rows are padded to 144 bytes so that
+// the 16-byte operand reads of 32 consecutive rows fall on distinct banks (the bank
+// conflict counter reads zero). Lane layout of the MFMA (checked on the hardware):
+// lane l supplies row l % 32 of A and column l % 32 of B at k = 8 (l / 32) .. + 7, and
+// holds result rows 8 (r / 4) + 4 (l / 32) + r % 4 of column l % 32 in accumulator
+// register r.
 //
 // Epilogue: the tile (bias added, rounded to bf16) is written to LDS and read back so
 // that each thread owns 16 consecutive columns of a row: two 16-byte stores of y (and
@@ -36,50 +40,105 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
-constexpr int kBM = 128, kBN = 128, kBK = 64;
-constexpr int kThreads = 256;
-constexpr int kLdsRow = kBK + 8;                  // bf16 per operand row in LDS (144 bytes)
-constexpr int kOpElems = kBM * kLdsRow;           // one operand buffer
-constexpr int kEpiRow = kBN + 8;                  // bf16 per row of the epilogue tile (272 bytes)
-constexpr int kLdsBytes = 2 * 2 * kOpElems * 2;   // two stages of A and B
-static_assert(kBM * kEpiRow * 2 <= kLdsBytes, "epilogue tile must fit in the operand buffers");
-static_assert(kBM == kBN, "the load mapping assumes square tiles");
+#ifndef LMBP_LIN_BM
+#define LMBP_LIN_BM 256  // block tile rows
+#endif
+#ifndef LMBP_LIN_BN
+#define LMBP_LIN_BN 256  // block tile columns
+#endif
+#ifndef LMBP_LIN_WM
+#define LMBP_LIN_WM 4    // waves along the rows of the tile
+#endif
+#ifndef LMBP_LIN_WN
+#define LMBP_LIN_WN 2    // waves along the columns
+#endif
+
+#ifndef LMBP_LIN_PREFETCH
+#define LMBP_LIN_PREFETCH 2  // K steps of global loads in flight ahead of the MFMAs (1 or 2)
+#endif
+#ifndef LMBP_LIN_BK
+#define LMBP_LIN_BK 64   // K step (a multiple of 16)
+#endif
+
+constexpr int kBM = LMBP_LIN_BM, kBN = LMBP_LIN_BN, kBK = LMBP_LIN_BK;
+constexpr int kWM = LMBP_LIN_WM, kWN = LMBP_LIN_WN;
+constexpr int kThreads = kWM * kWN * kWave;
+constexpr int kTM = kBM / kWM / 32;               // 32 x 32 MFMA tiles per wave, rows
+constexpr int kTN = kBN / kWN / 32;               // and columns
+constexpr int kLdsRow = kBK + 8;                  // bf16 per operand row in LDS (padded by 16 bytes)
+constexpr int kKChunks = kBK / 8;                 // 16-byte chunks per row and K step
+constexpr int kAElems = kBM * kLdsRow;            // one A buffer
+constexpr int kBElems = kBN * kLdsRow;            // one B buffer
+constexpr int kStageElems = kAElems + kBElems;
+constexpr int kEpiRow = kBN + 8;                  // bf16 per row of the epilogue tile
+// Two operand stages during the K loop; the epilogue tile reuses the same memory.
+constexpr int kLdsElems = (2 * kStageElems > kBM * kEpiRow) ? 2 * kStageElems : kBM * kEpiRow;
+static_assert(kBM % (kWM * 32) == 0 && kBN % (kWN * 32) == 0, "wave tiles are multiples of 32");
+constexpr int kChunksA = kBM * kBK / 8, kChunksB = kBN * kBK / 8;   // 16-byte chunks per step
+static_assert(kChunksA % kThreads == 0 && kChunksB % kThreads == 0, "chunks per thread");
+constexpr int kQA = kChunksA / kThreads, kQB = kChunksB / kThreads;
+constexpr int kRowStep = kThreads / kKChunks;     // rows covered by one pass of the threads
+static_assert((kThreads * 16) % kBN == 0, "epilogue mapping");
+constexpr int kEpiThreadsPerRow = kBN / 16;
+constexpr int kEpiRowStep = kThreads / kEpiThreadsPerRow;
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 
-// One K step of both operands, 16-byte chunks: chunk c = tid + 256 q (q < 4) is row
-// c / 8, k-chunk c % 8 of the 128 x 64 tile. Rows at or beyond `rows` and k beyond K
-// load zeros (K is a multiple of 8, so a chunk is wholly inside or outside).
+// One K step of both operands, 16-byte chunks: chunk c = tid + threads * q is row
+// c / (BK/8), k-chunk c % (BK/8) of the tile. Loads are raw buffer loads against a resource
+// that starts at the block's first row and ends after its last valid row, so rows
+// beyond the matrix read zeros with no branch; chunks beyond K (K is a multiple of 8,
+// so a chunk is wholly inside or outside) are pointed past the end to read zeros too.
 struct Stage {
-  u32x4 a[4], b[4];
+  u32x4 a[kQA], b[kQB];
 };
 
-__device__ inline void load_stage(Stage& st, const uint16_t* __restrict__ x,
-                                  const uint16_t* __restrict__ w, int64_t m0, int64_t n0,
-                                  int64_t M, int64_t N, int64_t K, int64_t k0) {
+struct Operands {
+  __amdgpu_buffer_rsrc_t x, w;
+  uint32_t xrow[kQA], wrow[kQB];  // byte offset of each chunk's row start
+};
+
+constexpr uint32_t kBufferGDword3 = 0x00020000;  // raw 32-bit buffer, gfx9 family
+constexpr uint32_t kOutOfRange = 0x80000000u;
+
+__device__ inline Operands make_operands(const uint16_t* x, const uint16_t* w, int64_t m0,
+                                         int64_t n0, int64_t M, int64_t N, int64_t K) {
+  Operands op;
+  const int64_t rows_x = (M - m0 < kBM) ? M - m0 : kBM;
+  const int64_t rows_w = (N - n0 < kBN) ? N - n0 : kBN;
+  op.x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(x) + m0 * K, 0,
+                                           int(rows_x * K * 2), kBufferGDword3);
+  op.w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w) + n0 * K, 0,
+                                           int(rows_w * K * 2), kBufferGDword3);
   const int tid = threadIdx.x;
-  const int kc = tid & 7;
-  const int64_t k = k0 + kc * 8;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int row = (tid >> 3) + 32 * q;
-    const bool kin = k < K;
-    st.a[q] = (kin && m0 + row < M) ? *reinterpret_cast<const u32x4*>(x + (m0 + row) * K + k)
-                                    : u32x4{0u, 0u, 0u, 0u};
-    st.b[q] = (kin && n0 + row < N) ? *reinterpret_cast<const u32x4*>(w + (n0 + row) * K + k)
-                                    : u32x4{0u, 0u, 0u, 0u};
-  }
+  for (int q = 0; q < kQA; ++q) op.xrow[q] = uint32_t((tid / kKChunks + kRowStep * q) * K * 2);
+#pragma unroll
+  for (int q = 0; q < kQB; ++q) op.wrow[q] = uint32_t((tid / kKChunks + kRowStep * q) * K * 2);
+  return op;
+}
+
+__device__ inline void load_stage(Stage& st, const Operands& op, int64_t K, int64_t k0) {
+  const int64_t k = k0 + (threadIdx.x % kKChunks) * 8;
+  const uint32_t kb = uint32_t(k * 2);
+  const bool kin = k < K;
+#pragma unroll
+  for (int q = 0; q < kQA; ++q)
+    st.a[q] = __builtin_amdgcn_raw_buffer_load_b128(op.x, kin ? op.xrow[q] + kb : kOutOfRange, 0, 0);
+#pragma unroll
+  for (int q = 0; q < kQB; ++q)
+    st.b[q] = __builtin_amdgcn_raw_buffer_load_b128(op.w, kin ? op.wrow[q] + kb : kOutOfRange, 0, 0);
 }
 
 __device__ inline void store_stage(const Stage& st, uint16_t* As, uint16_t* Bs) {
   const int tid = threadIdx.x;
-  const int kc = tid & 7;
+  const int kc = tid % kKChunks;
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int row = (tid >> 3) + 32 * q;
-    *reinterpret_cast<u32x4*>(As + row * kLdsRow + kc * 8) = st.a[q];
-    *reinterpret_cast<u32x4*>(Bs + row * kLdsRow + kc * 8) = st.b[q];
-  }
+  for (int q = 0; q < kQA; ++q)
+    *reinterpret_cast<u32x4*>(As + (tid / kKChunks + kRowStep * q) * kLdsRow + kc * 8) = st.a[q];
+#pragma unroll
+  for (int q = 0; q < kQB; ++q)
+    *reinterpret_cast<u32x4*>(Bs + (tid / kKChunks + kRowStep * q) * kLdsRow + kc * 8) = st.b[q];
 }
 
 // Tile coordinates of this block (see the file comment).
@@ -102,84 +161,113 @@ __global__ __launch_bounds__(kThreads) void linear_act_fwd_kernel(
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, uint32_t* __restrict__ codes,
     uint16_t* __restrict__ z, int64_t M, int64_t N, int64_t K) {
   using A = ActOf<ACT>;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[kLdsBytes / 2];
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / kWN, wn = wave % kWN;
 
   int64_t tm, tn;
   block_tile((M + kBM - 1) / kBM, (N + kBN - 1) / kBN, tm, tn);
   const int64_t m0 = tm * kBM, n0 = tn * kBN;
 
-  f32x16 acc[2][2];
+  f32x16 acc[kTM][kTN];
 #pragma unroll
-  for (int i = 0; i < 2; ++i)
+  for (int i = 0; i < kTM; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < kTN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
   const int64_t kt_count = (K + kBK - 1) / kBK;
-  Stage st;
-  if (kt_count > 0) {
-    load_stage(st, x, w, m0, n0, M, N, K, 0);
-    store_stage(st, lds, lds + 2 * kOpElems);
-  }
-  __syncthreads();
+  const Operands op = make_operands(x, w, m0, n0, M, N, K);
 
-  // Operand read offsets (in bf16 elements) inside one buffer.
-  const int a_off = (wm * 64 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
-  const int b_off = (wn * 64 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
+  // Operand read offsets (in bf16 elements) inside one stage.
+  const int a_off = (wm * kTM * 32 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
+  const int b_off = kAElems + (wn * kTN * 32 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
 
-  for (int64_t kt = 0; kt < kt_count; ++kt) {
-    const int cur = int(kt & 1);
-    const bool more = kt + 1 < kt_count;
-    if (more) load_stage(st, x, w, m0, n0, M, N, K, (kt + 1) * kBK);
-    const uint16_t* As = lds + cur * kOpElems;
-    const uint16_t* Bs = lds + (2 + cur) * kOpElems;
+  auto compute = [&](const uint16_t* S) {
 #pragma unroll
     for (int kk = 0; kk < kBK / 16; ++kk) {
-      bf16x8 a[2], b[2];
+      bf16x8 a[kTM], b[kTN];
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(As + a_off + i * 32 * kLdsRow + kk * 16);
+      for (int i = 0; i < kTM; ++i)
+        a[i] = *reinterpret_cast<const bf16x8*>(S + a_off + i * 32 * kLdsRow + kk * 16);
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(Bs + b_off + j * 32 * kLdsRow + kk * 16);
+      for (int j = 0; j < kTN; ++j)
+        b[j] = *reinterpret_cast<const bf16x8*>(S + b_off + j * 32 * kLdsRow + kk * 16);
 #pragma unroll
-      for (int i = 0; i < 2; ++i)
+      for (int i = 0; i < kTM; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int j = 0; j < kTN; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
     }
-    if (more) store_stage(st, lds + (1 - cur) * kOpElems, lds + (3 - cur) * kOpElems);
+  };
+  auto stage_ptr = [&](int64_t kt) { return lds + int(kt & 1) * kStageElems; };
+
+#if LMBP_LIN_PREFETCH == 2
+  // Two register stages: the loads of step kt + 2 are issued before the MFMAs of step
+  // kt, so they have two steps of MFMA work to arrive before they are written to LDS.
+  Stage s0, s1;
+  if (kt_count > 0) load_stage(s0, op, K, 0);
+  if (kt_count > 1) load_stage(s1, op, K, kBK);
+  if (kt_count > 0) store_stage(s0, lds, lds + kAElems);
+  __syncthreads();
+  auto step = [&](int64_t kt, Stage& free_regs, Stage& next_regs) {
+    if (kt + 2 < kt_count) load_stage(free_regs, op, K, (kt + 2) * kBK);
+    compute(stage_ptr(kt));
+    if (kt + 1 < kt_count) {
+      uint16_t* D = stage_ptr(kt + 1);
+      store_stage(next_regs, D, D + kAElems);
+    }
+    __syncthreads();
+  };
+  for (int64_t kt = 0; kt < kt_count; kt += 2) {
+    step(kt, s0, s1);
+    if (kt + 1 < kt_count) step(kt + 1, s1, s0);
+  }
+#else
+  // One register stage: the loads of step kt + 1 are in flight during the MFMAs of kt.
+  Stage st;
+  if (kt_count > 0) {
+    load_stage(st, op, K, 0);
+    store_stage(st, lds, lds + kAElems);
+  }
+  __syncthreads();
+  for (int64_t kt = 0; kt < kt_count; ++kt) {
+    const bool more = kt + 1 < kt_count;
+    if (more) load_stage(st, op, K, (kt + 1) * kBK);
+    compute(stage_ptr(kt));
+    if (more) {
+      uint16_t* D = stage_ptr(kt + 1);
+      store_stage(st, D, D + kAElems);
+    }
     __syncthreads();
   }
+#endif
 
   // Epilogue, part 1: bias, rounding to bf16, the tile into LDS (row-major, padded).
   uint16_t* E = lds;
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const int col = wn * 64 + j * 32 + (lane & 31);
+  for (int j = 0; j < kTN; ++j) {
+    const int col = wn * kTN * 32 + j * 32 + (lane & 31);
     const float bj = (bias != nullptr && n0 + col < N)
                          ? __uint_as_float(uint32_t(bias[n0 + col]) << 16) : 0.0f;
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < kTM; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = wm * 64 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        const int row = wm * kTM * 32 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
         E[row * kEpiRow + col] = uint16_t(pack_bf16x2(acc[i][j][r] + bj, 0.0f) & 0xffffu);
       }
   }
   __syncthreads();
 
-  // Part 2: thread owns columns c16 .. c16 + 15 of rows (tid / 8) + 32 g.
-  const int c16 = (tid & 7) * 16;
+  // Part 2: thread owns columns c16 .. c16 + 15 of rows tid / (BN/16) + step * g.
+  const int c16 = (tid % kEpiThreadsPerRow) * 16;
   if (n0 + c16 >= N) return;  // N is a multiple of 16: a group is wholly in or out
-#pragma unroll
-  for (int g = 0; g < 4; ++g) {
-    const int row = (tid >> 3) + 32 * g;
+#pragma unroll 2
+  for (int row = tid / kEpiThreadsPerRow; row < kBM; row += kEpiRowStep) {
     if (m0 + row >= M) break;
     const u32x4 v0 = *reinterpret_cast<const u32x4*>(E + row * kEpiRow + c16);
     const u32x4 v1 = *reinterpret_cast<const u32x4*>(E + row * kEpiRow + c16 + 8);
@@ -214,12 +302,19 @@ hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const
   auto* bp = static_cast<const uint16_t*>(bias);
   auto* yp = static_cast<uint16_t*>(y);
   auto* zp = static_cast<uint16_t*>(z);
-  if (act == kGelu)
-    hipLaunchKernelGGL(linear_act_fwd_kernel<kGelu>, dim3(unsigned(blocks)), dim3(kThreads), 0, s,
-                       xp, wp, bp, yp, codes, zp, M, N, K);
-  else
-    hipLaunchKernelGGL(linear_act_fwd_kernel<kSilu>, dim3(unsigned(blocks)), dim3(kThreads), 0, s,
-                       xp, wp, bp, yp, codes, zp, M, N, K);
+  const size_t lds = size_t(kLdsElems) * 2;
+  auto kern = act == kGelu ? linear_act_fwd_kernel<kGelu> : linear_act_fwd_kernel<kSilu>;
+  // More than 64 KiB of dynamic LDS must be allowed explicitly (once per kernel).
+  static hipError_t attr_gelu = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(linear_act_fwd_kernel<kGelu>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  static hipError_t attr_silu = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(linear_act_fwd_kernel<kSilu>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  const hipError_t attr = act == kGelu ? attr_gelu : attr_silu;
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL(kern, dim3(unsigned(blocks)), dim3(kThreads), lds, s, xp, wp, bp, yp, codes,
+                     zp, M, N, K);
   return hipGetLastError();
 }
 
