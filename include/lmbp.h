@@ -183,7 +183,7 @@ lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void *dz,
  *   act    : LMBP_ACT_GELU (ReGELU2) or LMBP_ACT_SILU (ReSiLU2).
  *   m,n,k  : x is m x k, w is n x k (the weight of a linear layer, row-major), y and
  *            z are m x n. n must be a multiple of 16 (each row of codes fills whole
- *            words) and k a multiple of 8 with k <= 2^22; m, n >= 0, k >= 0 (k == 0
+ *            words) and k a multiple of 8 with k <= 2^21; m, n >= 0, k >= 0 (k == 0
  *            gives z = b).
  *   x, w, y, z : 16-byte aligned.
  *   bias   : n bf16 values, or NULL for none.

@@ -12,15 +12,17 @@
 // Tiling (defaults; measured best of the shapes tried on the LLaMA-7B gate and ViT-B
 // MLP projections): a 512-thread block computes a 256 x 256 tile of z, its eight waves
 // (4 along the rows, 2 along the columns) a 64 x 128 part each as 2 x 4 MFMA tiles of
-// 32 x 32, accumulators in registers. K advances in steps of 64 through two LDS
-// buffers per operand; global loads run two steps ahead of the MFMAs (two register
-// stages), as raw buffer loads whose range ends at the tile's last valid row, so
-// ragged tiles read zeros without branches. LDS rows are padded to 144 bytes so that
-// the 16-byte operand reads of 32 consecutive rows fall on distinct banks (the bank
-// conflict counter reads zero). Lane layout of the MFMA (checked on the hardware):
-// lane l supplies row l % 32 of A and column l % 32 of B at k = 8 (l / 32) .. + 7, and
-// holds result rows 8 (r / 4) + 4 (l / 32) + r % 4 of column l % 32 in accumulator
-// register r.
+// 32 x 32, accumulators in registers. K advances in steps of 32 through a ring of four
+// LDS stages filled straight from HBM by raw buffer loads with an LDS destination
+// (buffer_load_dwordx4 ... lds): three steps of loads are in flight ahead of the MFMAs
+// and no register staging is needed. The buffer resources end at the tile's last valid
+// row, so ragged tiles read zeros without branches. Each stage row is 64 bytes with an
+// XOR swizzle of its four 16-byte units so that the operand reads of 16 consecutive
+// rows hit distinct LDS banks. (A register-staged variant with padded rows and a
+// two-step prefetch, LMBP_LIN_DIRECT=0, measured ~10% slower.) Lane layout of the MFMA
+// (checked on the hardware): lane l supplies row l % 32 of A and column l % 32 of B at
+// k = 8 (l / 32) .. + 7, and holds result rows 8 (r / 4) + 4 (l / 32) + r % 4 of column
+// l % 32 in accumulator register r.
 //
 // Epilogue: the tile (bias added, rounded to bf16) is written to LDS and read back so
 // that each thread owns 16 consecutive columns of a row: two 16-byte stores of y (and
@@ -56,8 +58,18 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 #ifndef LMBP_LIN_PREFETCH
 #define LMBP_LIN_PREFETCH 2  // K steps of global loads in flight ahead of the MFMAs (1 or 2)
 #endif
+#ifndef LMBP_LIN_DIRECT
+#define LMBP_LIN_DIRECT 1  // 1: operands go from HBM straight to LDS (buffer_load ... lds)
+#endif
+#ifndef LMBP_LIN_STAGES
+#define LMBP_LIN_STAGES 4  // LDS stages of the direct path
+#endif
 #ifndef LMBP_LIN_BK
+#if LMBP_LIN_DIRECT
+#define LMBP_LIN_BK 32   // the direct path's swizzle is laid out for 64-byte rows
+#else
 #define LMBP_LIN_BK 64   // K step (a multiple of 16)
+#endif
 #endif
 
 constexpr int kBM = LMBP_LIN_BM, kBN = LMBP_LIN_BN, kBK = LMBP_LIN_BK;
@@ -71,8 +83,18 @@ constexpr int kAElems = kBM * kLdsRow;            // one A buffer
 constexpr int kBElems = kBN * kLdsRow;            // one B buffer
 constexpr int kStageElems = kAElems + kBElems;
 constexpr int kEpiRow = kBN + 8;                  // bf16 per row of the epilogue tile
-// Two operand stages during the K loop; the epilogue tile reuses the same memory.
-constexpr int kLdsElems = (2 * kStageElems > kBM * kEpiRow) ? 2 * kStageElems : kBM * kEpiRow;
+#if LMBP_LIN_DIRECT
+// Direct path: unpadded 64-byte rows (BK = 32) with an XOR swizzle of the 16-byte units.
+static_assert(kBK == 32, "the direct path is laid out for K steps of 32");
+constexpr int kStages = LMBP_LIN_STAGES;
+constexpr int kDStageElems = (kBM + kBN) * kBK;
+constexpr int kOperandElems = kStages * kDStageElems;
+#else
+// Two operand stages during the K loop.
+constexpr int kOperandElems = 2 * kStageElems;
+#endif
+// The epilogue tile reuses the operand memory.
+constexpr int kLdsElems = (kOperandElems > kBM * kEpiRow) ? kOperandElems : kBM * kEpiRow;
 static_assert(kBM % (kWM * 32) == 0 && kBN % (kWN * 32) == 0, "wave tiles are multiples of 32");
 constexpr int kChunksA = kBM * kBK / 8, kChunksB = kBN * kBK / 8;   // 16-byte chunks per step
 static_assert(kChunksA % kThreads == 0 && kChunksB % kThreads == 0, "chunks per thread");
@@ -182,6 +204,89 @@ __global__ __launch_bounds__(kThreads) void linear_act_fwd_kernel(
   const int64_t kt_count = (K + kBK - 1) / kBK;
   const Operands op = make_operands(x, w, m0, n0, M, N, K);
 
+#if LMBP_LIN_DIRECT
+  // Direct path. A stage holds the A tile (BM rows) then the B tile (BN rows), each
+  // row 32 bf16 = four 16-byte units; unit u of row r holds k-chunk u ^ ((r >> 2) & 3),
+  // so that the operand reads of 16 consecutive rows at one k-chunk hit 16 distinct
+  // bank groups. One load instruction of a wave fills 1 KiB (16 rows): lane l writes
+  // unit l % 4 of row l / 4, i.e. fetches k-chunk (l % 4) ^ ((row >> 2) & 3) of that
+  // row (each row's four lanes read its 64 contiguous bytes in permuted order).
+  constexpr int kWaves = kWM * kWN;
+  constexpr int kBlocksA = kBM / 16, kBlocksB = kBN / 16;
+  static_assert(kBlocksA % kWaves == 0 && kBlocksB % kWaves == 0, "load blocks per wave");
+  constexpr int kLA = kBlocksA / kWaves, kLB = kBlocksB / kWaves;
+  constexpr int kLoadsPerStage = kLA + kLB;
+  typedef __attribute__((address_space(3))) void lds_void;
+  uint32_t ld_a[kLA], ld_b[kLB];  // byte offset in the operand (row start + chunk), k step 0
+  {
+    const int r_in = lane >> 2;
+    const int kc = (lane & 3) ^ ((r_in >> 2) & 3);   // block rows start at multiples of 16
+#pragma unroll
+    for (int q = 0; q < kLA; ++q)
+      ld_a[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+#pragma unroll
+    for (int q = 0; q < kLB; ++q)
+      ld_b[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+  }
+  const uint32_t kc_bytes = uint32_t(((lane & 3) ^ (((lane >> 2) >> 2) & 3)) * 16);
+  auto issue_stage = [&](int64_t kt) {
+    uint16_t* S = lds + int(kt % kStages) * kDStageElems;
+    const uint32_t k0b = uint32_t(kt * kBK * 2);
+    const bool kin = kt * kBK + int64_t(kc_bytes / 2) < K;
+#pragma unroll
+    for (int q = 0; q < kLA; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          op.x, (lds_void*)(S + (wave + kWaves * q) * 16 * kBK), 16,
+          kin ? ld_a[q] + k0b : kOutOfRange, 0, 0, 0);
+#pragma unroll
+    for (int q = 0; q < kLB; ++q)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(
+          op.w, (lds_void*)(S + kBM * kBK + (wave + kWaves * q) * 16 * kBK), 16,
+          kin ? ld_b[q] + k0b : kOutOfRange, 0, 0, 0);
+  };
+  // Operand reads: lane l reads row (base + l % 32), k-chunk 2 kk + l / 32.
+  const int swz = ((lane & 31) >> 2) & 3;   // (row >> 2) & 3; wave rows start at multiples of 32
+  int a_row[kTM], b_row[kTN];
+#pragma unroll
+  for (int i = 0; i < kTM; ++i) a_row[i] = (wm * kTM * 32 + i * 32 + (lane & 31)) * kBK;
+#pragma unroll
+  for (int j = 0; j < kTN; ++j) b_row[j] = kBM * kBK + (wn * kTN * 32 + j * 32 + (lane & 31)) * kBK;
+  auto compute = [&](const uint16_t* S) {
+#pragma unroll
+    for (int kk = 0; kk < kBK / 16; ++kk) {
+      const int unit = ((2 * kk + (lane >> 5)) ^ swz) * 8;
+      bf16x8 a[kTM], b[kTN];
+#pragma unroll
+      for (int i = 0; i < kTM; ++i) a[i] = *reinterpret_cast<const bf16x8*>(S + a_row[i] + unit);
+#pragma unroll
+      for (int j = 0; j < kTN; ++j) b[j] = *reinterpret_cast<const bf16x8*>(S + b_row[j] + unit);
+#pragma unroll
+      for (int i = 0; i < kTM; ++i)
+#pragma unroll
+        for (int j = 0; j < kTN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+  };
+  // Wait until at most `pending` stages of this wave's loads are outstanding (the
+  // vector-memory counter counts the direct loads; nothing else uses it in the loop).
+  auto wait_stages = [&](int64_t pending) {
+    static_assert(kStages - 2 <= 3, "wait table");
+    if (pending <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    else if (pending == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kLoadsPerStage) : "memory");
+    else if (pending == 2) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * kLoadsPerStage) : "memory");
+    else asm volatile("s_waitcnt vmcnt(%0)" :: "n"(3 * kLoadsPerStage) : "memory");
+  };
+  for (int s = 0; s < kStages - 1; ++s)
+    if (s < kt_count) issue_stage(s);
+  for (int64_t kt = 0; kt < kt_count; ++kt) {
+    const int64_t issued_after = (kt_count - 1 - kt < kStages - 2) ? kt_count - 1 - kt : kStages - 2;
+    wait_stages(issued_after);
+    asm volatile("s_barrier" ::: "memory");   // every wave's loads of step kt are in LDS
+    if (kt + kStages - 1 < kt_count) issue_stage(kt + kStages - 1);   // into step kt - 1's buffer
+    compute(lds + int(kt % kStages) * kDStageElems);
+  }
+  __syncthreads();
+#else
   // Operand read offsets (in bf16 elements) inside one stage.
   const int a_off = (wm * kTM * 32 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
   const int b_off = kAElems + (wn * kTN * 32 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
@@ -245,6 +350,7 @@ __global__ __launch_bounds__(kThreads) void linear_act_fwd_kernel(
     __syncthreads();
   }
 #endif
+#endif  // LMBP_LIN_DIRECT
 
   // Epilogue, part 1: bias, rounding to bf16, the tile into LDS (row-major, padded).
   uint16_t* E = lds;

@@ -244,7 +244,7 @@ lmbp_status linear_act_fwd_impl(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t 
   if (act != LMBP_ACT_GELU && act != LMBP_ACT_SILU) return LMBP_EINVAL;
   const int64_t lim = int64_t(1) << 31;
   if (m < 0 || n < 0 || k < 0 || m >= lim || n >= lim || k >= lim) return LMBP_EINVAL;
-  if (n % 16 != 0 || k % 8 != 0 || k > (int64_t(1) << 22)) return LMBP_EINVAL;
+  if (n % 16 != 0 || k % 8 != 0 || k > (int64_t(1) << 21)) return LMBP_EINVAL;
   if (m == 0 || n == 0) return LMBP_OK;
   if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
   if (!y || !codes || (k > 0 && (!x || !w))) return LMBP_EINVAL;

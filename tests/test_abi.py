@@ -136,7 +136,7 @@ def test_linear_act_errors(L):
     assert f(G, B.BF16, -1, 32, 16, x, w, bias, y, c, z, None) == B.EINVAL
     assert f(G, B.BF16, 4, 24, 16, x, w, bias, y, c, z, None) == B.EINVAL     # n % 16
     assert f(G, B.BF16, 4, 32, 12, x, w, bias, y, c, z, None) == B.EINVAL     # k % 8
-    assert f(G, B.BF16, 4, 32, (1 << 22) + 8, x, w, bias, y, c, z, None) == B.EINVAL  # k limit
+    assert f(G, B.BF16, 4, 32, (1 << 21) + 8, x, w, bias, y, c, z, None) == B.EINVAL  # k limit
     assert f(G, B.BF16, 0, 32, 16, x, w, bias, y, c, z, None) == B.OK         # empty
     assert f(G, B.BF16, 4, 0, 16, x, w, bias, y, c, z, None) == B.OK
     assert f(G, B.BF16, 4, 32, 16, x, w, bias, None, c, z, None) == B.EINVAL
