@@ -7,12 +7,17 @@
 * ``MSLayerNorm`` / ``MSRMSNorm``: parameter-free norms (Sec. 5.2, Appendix G) that save
   only their output z and one fp32 rstd per row. z is the same tensor the following
   linear layer saves as its input, so autograd keeps one copy (memory sharing).
+* ``LinearReGELU2`` / ``LinearReSiLU2``: a bf16 linear layer followed by the activation,
+  forward fused into one kernel (the pre-activation is never stored); saves x (for the
+  weight gradient) and the codes. Backward: dz = dy * slope[code] by the activation
+  kernel, then the two products of a linear layer's backward (library GEMMs).
 * ``merge_norm_into_linears``: folds a norm's affine (alpha, beta) into the linear layers
   that consume its output, W~ = W diag(alpha), b~ = W beta + b (Sec. 5.2), and returns
   the parameter-free MS norm to use in its place.
 
-Every forward and backward runs in the HIP kernels through ``binding``; the only torch
-arithmetic here is the one-time weight merge.
+Every forward and backward runs in the HIP kernels through ``binding``, except the two
+matrix products of the fused linear layer's backward (torch's library GEMMs) and the
+one-time weight merge.
 """
 
 import torch
@@ -72,6 +77,51 @@ class _MSNorm(torch.autograd.Function):
         z, rstd = ctx.saved_tensors
         bwd = binding.msln_bwd if ctx.centered else binding.msrms_bwd
         return bwd(_flat(dz), z, rstd), None, None
+
+
+class _LinearAct(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, weight, bias, which):
+        x2 = _flat(x).reshape(-1, x.shape[-1])
+        y, codes = binding.linear_act_fwd(x2, _flat(weight), None if bias is None else _flat(bias),
+                                          act=which)
+        ctx.which = which
+        ctx.has_bias = bias is not None
+        ctx.x_shape = x.shape
+        ctx.save_for_backward(x2, weight, codes)
+        return y.reshape(*x.shape[:-1], weight.shape[0])
+
+    @staticmethod
+    def backward(ctx, dy):
+        x2, weight, codes = ctx.saved_tensors
+        bwd = binding.regelu2_bwd if ctx.which == "gelu" else binding.resilu2_bwd
+        dz = bwd(_flat(dy).reshape(-1, weight.shape[0]), codes)
+        dx = (dz @ weight).reshape(ctx.x_shape) if ctx.needs_input_grad[0] else None
+        dw = (dz.t().contiguous() @ x2) if ctx.needs_input_grad[1] else None
+        db = dz.float().sum(0).to(dz.dtype) if ctx.has_bias and ctx.needs_input_grad[2] else None
+        return dx, dw, db, None
+
+
+class _LinearActModule(nn.Linear):
+    """bf16 nn.Linear whose output goes through the activation, fused. Output features
+    must be a multiple of 16, input features a multiple of 8."""
+    which = None
+
+    def __init__(self, in_features, out_features, bias=True, device=None, dtype=torch.bfloat16):
+        super().__init__(in_features, out_features, bias=bias, device=device, dtype=dtype)
+
+    def forward(self, x):
+        return _LinearAct.apply(x, self.weight, self.bias, self.which)
+
+
+class LinearReGELU2(_LinearActModule):
+    """GELU(x W^T + b) with ReGELU2's backward (Sec. 4.2), forward fused in one kernel."""
+    which = "gelu"
+
+
+class LinearReSiLU2(_LinearActModule):
+    """SiLU(x W^T + b) with ReSiLU2's backward (Sec. 4.2), forward fused in one kernel."""
+    which = "silu"
 
 
 class ReGELU2(nn.Module):

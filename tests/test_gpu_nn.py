@@ -113,3 +113,33 @@ def test_activation_saves_only_codes():
         ReSiLU2()(x)
     assert len(saved) == 1 and saved[0].dtype == torch.int32
     assert saved[0].numel() * 4 == x.numel() // 4   # 2 bits per element
+
+
+@pytest.mark.parametrize("which", ["gelu", "silu"])
+def test_fused_linear_act_module(which):
+    """LinearReGELU2 / LinearReSiLU2 against the oracle: forward (stored z rounding, y),
+    and the Approx-BP gradients dx = (dy * slope[code(z)]) W, dW = (dy * slope)^T x,
+    db = sum(dy * slope), computed in fp64 from the oracle's codes of the rounded z.
+    Dyadic inputs make the GPU's fp32 accumulation of z exact, so the codes agree."""
+    from paper_2406_16282_amd.nn import LinearReGELU2, LinearReSiLU2
+    m, k, n = 96, 64, 160
+    x = inputs.dyadic((m, k), -3, tensor_id=inputs.LIN_X)
+    w = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_W)
+    b = inputs.dyadic((n,), -7, tensor_id=inputs.LIN_B)
+    dy = inputs.normal((m, n), 1.0, "bf16", tensor_id=inputs.ACT_DY)
+    mod = (LinearReGELU2 if which == "gelu" else LinearReSiLU2)(k, n, device=DEV)
+    with torch.no_grad():
+        mod.weight.copy_(T(w))
+        mod.bias.copy_(T(b))
+    xt = T(x, True)
+    y = mod(xt)
+    y.backward(T(dy))
+    _, z_s, y_o, c_o = oracle.linear_act_fwd(x, w, b, which)
+    assert_rel(oracle.decode(H(y), "bf16"), y_o, 1e-2, "fused module y")
+    obwd = oracle.regelu2_bwd if which == "gelu" else oracle.resilu2_bwd
+    dz = oracle.decode(oracle.encode(obwd(oracle.decode(dy, "bf16"), c_o), "bf16"), "bf16")
+    xd, wd = oracle.decode(x, "bf16"), oracle.decode(w, "bf16")
+    assert_mixed(oracle.decode(H(xt.grad), "bf16"), dz @ wd, 2e-2, "fused module dx")
+    assert_mixed(oracle.decode(H(mod.weight.grad), "bf16"), dz.T @ xd, 2e-2, "fused module dW")
+    assert_mixed(oracle.decode(H(mod.bias.grad), "bf16").reshape(1, -1), dz.sum(0).reshape(1, -1),
+                 2e-2, "fused module db")
