@@ -231,21 +231,29 @@ def linear_report(torch, lmbp, inputs, dev, reps):
     """Fused linear + ReGELU2 / ReSiLU2 forward against the unfused sequence (library
     GEMM through torch, i.e. hipBLASLt, writing z, then the activation kernel reading
     it), on the ViT-B and LLaMA-7B MLP shapes. Durations: HIP events around `reps`
-    back-to-back launches on the current stream."""
+    back-to-back launches on the current stream, median of five trials interleaved
+    across the four variants after a warm-up of the same length."""
     out = {}
     mk = lambda: torch.cuda.Event(enable_timing=True)
 
-    def timed(fn):
-        for _ in range(3):
-            fn()
+    def timed_all(fns, trials=5):
+        """Median over `trials` of the mean duration of `reps` back-to-back launches,
+        the trials of the callables interleaved (so clock drift affects all alike)."""
+        for fn in fns:             # warm-up: the clocks ramp up under load
+            for _ in range(reps):
+                fn()
         torch.cuda.synchronize()
-        a, b = mk(), mk()
-        a.record()
-        for _ in range(reps):
-            fn()
-        b.record()
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) * 1e3 / reps
+        res = [[] for _ in fns]
+        for _ in range(trials):
+            for i, fn in enumerate(fns):
+                a, b = mk(), mk()
+                a.record()
+                for _ in range(reps):
+                    fn()
+                b.record()
+                torch.cuda.synchronize()
+                res[i].append(a.elapsed_time(b) * 1e3 / reps)
+        return [float(np.median(r)) for r in res]
 
     for name, (m, n, k, act, has_bias) in LINEAR_SHAPES.items():
         T = lambda a: inputs.storage_to_torch(a, dev)
@@ -264,10 +272,12 @@ def linear_report(torch, lmbp, inputs, dev, reps):
             else:
                 torch.addmm(b, x, wt, out=z)
 
-        t_fused = timed(lambda: lmbp.linear_act_fwd(x, w, b, act=act, y=y, codes=codes))
-        t_gemm = timed(gemm)
-        t_act = timed(lambda: afwd(z, y=y, codes=codes))
-        t_unfused = timed(lambda: (gemm(), afwd(z, y=y, codes=codes)))
+        t_fused, t_gemm, t_act, t_unfused = timed_all([
+            lambda: lmbp.linear_act_fwd(x, w, b, act=act, y=y, codes=codes),
+            gemm,
+            lambda: afwd(z, y=y, codes=codes),
+            lambda: (gemm(), afwd(z, y=y, codes=codes)),
+        ])
         flops = 2.0 * m * n * k
         tf = flops / (t_fused * 1e-6) / 1e12
         out[name] = {

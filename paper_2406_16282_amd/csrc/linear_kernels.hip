@@ -9,18 +9,26 @@
 // the caller asks for it: ReGELU2 / ReSiLU2 keep only the codes for the backward
 // pass, so the pre-activation never has to reach HBM.
 //
-// Tiling (defaults; measured best of the shapes tried on the LLaMA-7B gate and ViT-B
-// MLP projections): a 512-thread block computes a 256 x 256 tile of z, its eight waves
-// (4 along the rows, 2 along the columns) a 64 x 128 part each as 2 x 4 MFMA tiles of
-// 32 x 32, accumulators in registers. K advances in steps of 32 through a ring of four
-// LDS stages filled straight from HBM by raw buffer loads with an LDS destination
-// (buffer_load_dwordx4 ... lds): three steps of loads are in flight ahead of the MFMAs
-// and no register staging is needed. The buffer resources end at the tile's last valid
-// row, so ragged tiles read zeros without branches. Each stage row is 64 bytes with an
-// XOR swizzle of its four 16-byte units so that the operand reads of 16 consecutive
-// rows hit distinct LDS banks. (A register-staged variant with padded rows and a
-// two-step prefetch, LMBP_LIN_DIRECT=0, measured ~10% slower.) Lane layout of the MFMA
-// (checked on the hardware): lane l supplies row l % 32 of A and column l % 32 of B at
+// Tiling. A block computes a BM x BN tile of z with WM x WN waves, each a
+// (BM/WM) x (BN/WN) part as 32 x 32 MFMA tiles, accumulators in registers. Two tile
+// configurations are compiled and chosen per problem (launcher): 256 x 256 with 8 waves
+// of 128 x 64 for large problems, 128 x 128 with 4 waves of 64 x 64 (two blocks per CU)
+// when the large tiles would leave much of the last round of the GPU idle.
+//
+// K loop. K advances in steps of 32 through a ring of four LDS stages filled straight
+// from HBM by raw buffer loads with an LDS destination (buffer_load_dwordx4 ... lds):
+// up to four steps of loads are in flight and no register staging is needed. The
+// buffer resources end at the tile's last valid row, so ragged tiles read zeros
+// without branches, and chunks beyond K are pointed past the end to read zeros too.
+// A stage row is 32 bf16 = four 16-byte units, unit u of row r holding k-chunk
+// u ^ ((r >> 2) & 3), so that the operand reads of 16 consecutive rows at one k-chunk
+// hit distinct LDS banks; one load instruction of a wave fills 1 KiB (16 rows), lane l
+// writing unit l % 4 of row l / 4 (the row's four lanes read its 64 contiguous bytes in
+// permuted order). Within the loop the fragments of the next K slice (16) are read into
+// their own registers before the MFMAs of the current one, across step boundaries too;
+// the loop body is branch-free (loads past the last step read zeros into spent
+// buffers) so that the compiler's LDS waits are exact. Lane layout of the MFMA (checked
+// on the hardware): lane l supplies row l % 32 of A and column l % 32 of B at
 // k = 8 (l / 32) .. + 7, and holds result rows 8 (r / 4) + 4 (l / 32) + r % 4 of column
 // l % 32 in accumulator register r.
 //
@@ -37,130 +45,58 @@
 #include "lmbp_launch.hpp"
 
 namespace lmbp {
-namespace {
+namespace lin {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
 
-#ifndef LMBP_LIN_BM
-#define LMBP_LIN_BM 256  // block tile rows
-#endif
-#ifndef LMBP_LIN_BN
-#define LMBP_LIN_BN 256  // block tile columns
-#endif
-#ifndef LMBP_LIN_WM
-#define LMBP_LIN_WM 4    // waves along the rows of the tile
-#endif
-#ifndef LMBP_LIN_WN
-#define LMBP_LIN_WN 2    // waves along the columns
-#endif
-
-#ifndef LMBP_LIN_PREFETCH
-#define LMBP_LIN_PREFETCH 2  // K steps of global loads in flight ahead of the MFMAs (1 or 2)
-#endif
-#ifndef LMBP_LIN_DIRECT
-#define LMBP_LIN_DIRECT 1  // 1: operands go from HBM straight to LDS (buffer_load ... lds)
-#endif
-#ifndef LMBP_LIN_STAGES
-#define LMBP_LIN_STAGES 4  // LDS stages of the direct path
-#endif
-#ifndef LMBP_LIN_BK
-#if LMBP_LIN_DIRECT
-#define LMBP_LIN_BK 32   // the direct path's swizzle is laid out for 64-byte rows
-#else
-#define LMBP_LIN_BK 64   // K step (a multiple of 16)
-#endif
-#endif
-
-constexpr int kBM = LMBP_LIN_BM, kBN = LMBP_LIN_BN, kBK = LMBP_LIN_BK;
-constexpr int kWM = LMBP_LIN_WM, kWN = LMBP_LIN_WN;
-constexpr int kThreads = kWM * kWN * kWave;
-constexpr int kTM = kBM / kWM / 32;               // 32 x 32 MFMA tiles per wave, rows
-constexpr int kTN = kBN / kWN / 32;               // and columns
-constexpr int kLdsRow = kBK + 8;                  // bf16 per operand row in LDS (padded by 16 bytes)
-constexpr int kKChunks = kBK / 8;                 // 16-byte chunks per row and K step
-constexpr int kAElems = kBM * kLdsRow;            // one A buffer
-constexpr int kBElems = kBN * kLdsRow;            // one B buffer
-constexpr int kStageElems = kAElems + kBElems;
-constexpr int kEpiRow = kBN + 8;                  // bf16 per row of the epilogue tile
-#if LMBP_LIN_DIRECT
-// Direct path: unpadded 64-byte rows (BK = 32) with an XOR swizzle of the 16-byte units.
-static_assert(kBK == 32, "the direct path is laid out for K steps of 32");
-constexpr int kStages = LMBP_LIN_STAGES;
-constexpr int kDStageElems = (kBM + kBN) * kBK;
-constexpr int kOperandElems = kStages * kDStageElems;
-#else
-// Two operand stages during the K loop.
-constexpr int kOperandElems = 2 * kStageElems;
-#endif
-// The epilogue tile reuses the operand memory.
-constexpr int kLdsElems = (kOperandElems > kBM * kEpiRow) ? kOperandElems : kBM * kEpiRow;
-static_assert(kBM % (kWM * 32) == 0 && kBN % (kWN * 32) == 0, "wave tiles are multiples of 32");
-constexpr int kChunksA = kBM * kBK / 8, kChunksB = kBN * kBK / 8;   // 16-byte chunks per step
-static_assert(kChunksA % kThreads == 0 && kChunksB % kThreads == 0, "chunks per thread");
-constexpr int kQA = kChunksA / kThreads, kQB = kChunksB / kThreads;
-constexpr int kRowStep = kThreads / kKChunks;     // rows covered by one pass of the threads
-static_assert((kThreads * 16) % kBN == 0, "epilogue mapping");
-constexpr int kEpiThreadsPerRow = kBN / 16;
-constexpr int kEpiRowStep = kThreads / kEpiThreadsPerRow;
+constexpr int kBK = 32;       // K step: one LDS stage row is 64 bytes
+constexpr int kStages = 4;    // LDS ring
+constexpr int kSlices = kBK / 16;
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
-
-// One K step of both operands, 16-byte chunks: chunk c = tid + threads * q is row
-// c / (BK/8), k-chunk c % (BK/8) of the tile. Loads are raw buffer loads against a resource
-// that starts at the block's first row and ends after its last valid row, so rows
-// beyond the matrix read zeros with no branch; chunks beyond K (K is a multiple of 8,
-// so a chunk is wholly inside or outside) are pointed past the end to read zeros too.
-struct Stage {
-  u32x4 a[kQA], b[kQB];
-};
-
-struct Operands {
-  __amdgpu_buffer_rsrc_t x, w;
-  uint32_t xrow[kQA], wrow[kQB];  // byte offset of each chunk's row start
-};
-
 constexpr uint32_t kBufferGDword3 = 0x00020000;  // raw 32-bit buffer, gfx9 family
-constexpr uint32_t kOutOfRange = 0x80000000u;
+constexpr uint32_t kOutOfRange = 0x80000000u;    // beyond any resource's range: reads 0
 
-__device__ inline Operands make_operands(const uint16_t* x, const uint16_t* w, int64_t m0,
-                                         int64_t n0, int64_t M, int64_t N, int64_t K) {
-  Operands op;
-  const int64_t rows_x = (M - m0 < kBM) ? M - m0 : kBM;
-  const int64_t rows_w = (N - n0 < kBN) ? N - n0 : kBN;
-  op.x = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(x) + m0 * K, 0,
-                                           int(rows_x * K * 2), kBufferGDword3);
-  op.w = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w) + n0 * K, 0,
-                                           int(rows_w * K * 2), kBufferGDword3);
-  const int tid = threadIdx.x;
-#pragma unroll
-  for (int q = 0; q < kQA; ++q) op.xrow[q] = uint32_t((tid / kKChunks + kRowStep * q) * K * 2);
-#pragma unroll
-  for (int q = 0; q < kQB; ++q) op.wrow[q] = uint32_t((tid / kKChunks + kRowStep * q) * K * 2);
-  return op;
+template <int BM_, int BN_, int WM_, int WN_>
+struct Tile {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int kWaves = WM * WN;
+  static constexpr int kThreads = kWaves * kWave;
+  static constexpr int TM = BM / WM / 32, TN = BN / WN / 32;   // MFMA tiles per wave
+  static constexpr int kStageElems = (BM + BN) * kBK;
+  static constexpr int kEpiRow = BN + 8;                        // padded epilogue row
+  static constexpr int kOperandElems = kStages * kStageElems;
+  static constexpr int kLdsElems =
+      (kOperandElems > BM * kEpiRow) ? kOperandElems : BM * kEpiRow;
+  static constexpr int kLA = BM / 16 / kWaves, kLB = BN / 16 / kWaves;  // loads per stage
+  static constexpr int kLoadsPerStage = kLA + kLB;
+  static constexpr int kEpiThreadsPerRow = BN / 16;
+  static constexpr int kEpiRowStep = kThreads / kEpiThreadsPerRow;
+  static_assert(BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tiles are multiples of 32");
+  static_assert((BM / 16) % kWaves == 0 && (BN / 16) % kWaves == 0, "load blocks per wave");
+  static_assert(kThreads % kEpiThreadsPerRow == 0, "epilogue mapping");
+  static_assert(kLdsElems * 2 <= 160 * 1024, "LDS per block");
+  static_assert((kStages - 1) * kLoadsPerStage <= 63, "vector-memory counter range");
+};
+
+using BigTile = Tile<256, 256, 2, 4>;
+using SmallTile = Tile<128, 128, 2, 2>;
+
+// The target builtins below are wrapped in device functions: used directly in the body of
+// a kernel template, they make the host-side instantiation fail silently and the launch
+// stub is never emitted.
+
+// A raw buffer resource over `bytes` bytes at `base` (reads beyond return zeros).
+__device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, int64_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), 0, int(bytes),
+                                           kBufferGDword3);
 }
 
-__device__ inline void load_stage(Stage& st, const Operands& op, int64_t K, int64_t k0) {
-  const int64_t k = k0 + (threadIdx.x % kKChunks) * 8;
-  const uint32_t kb = uint32_t(k * 2);
-  const bool kin = k < K;
-#pragma unroll
-  for (int q = 0; q < kQA; ++q)
-    st.a[q] = __builtin_amdgcn_raw_buffer_load_b128(op.x, kin ? op.xrow[q] + kb : kOutOfRange, 0, 0);
-#pragma unroll
-  for (int q = 0; q < kQB; ++q)
-    st.b[q] = __builtin_amdgcn_raw_buffer_load_b128(op.w, kin ? op.wrow[q] + kb : kOutOfRange, 0, 0);
-}
-
-__device__ inline void store_stage(const Stage& st, uint16_t* As, uint16_t* Bs) {
-  const int tid = threadIdx.x;
-  const int kc = tid % kKChunks;
-#pragma unroll
-  for (int q = 0; q < kQA; ++q)
-    *reinterpret_cast<u32x4*>(As + (tid / kKChunks + kRowStep * q) * kLdsRow + kc * 8) = st.a[q];
-#pragma unroll
-  for (int q = 0; q < kQB; ++q)
-    *reinterpret_cast<u32x4*>(Bs + (tid / kKChunks + kRowStep * q) * kLdsRow + kc * 8) = st.b[q];
+// 16 bytes per lane from the buffer into LDS at `dst` + lane * 16 (dst wave-uniform).
+__device__ inline void load_lds16(__amdgpu_buffer_rsrc_t r, uint16_t* dst, uint32_t offset) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, offset, 0, 0, 0);
 }
 
 // Tile coordinates of this block (see the file comment).
@@ -177,206 +113,151 @@ __device__ inline void block_tile(int64_t tiles_m, int64_t tiles_n, int64_t& tm,
   tn = r / gsize;
 }
 
-template <int ACT>
-__global__ __launch_bounds__(kThreads) void linear_act_fwd_kernel(
+template <class C, int ACT>
+__global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
     const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
     const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, uint32_t* __restrict__ codes,
     uint16_t* __restrict__ z, int64_t M, int64_t N, int64_t K) {
   using A = ActOf<ACT>;
+  constexpr int BM = C::BM, BN = C::BN, TM = C::TM, TN = C::TN, kWaves = C::kWaves;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wave = tid / kWave;
-  const int wm = wave / kWN, wn = wave % kWN;
+  const int wm = wave / C::WN, wn = wave % C::WN;
 
   int64_t tm, tn;
-  block_tile((M + kBM - 1) / kBM, (N + kBN - 1) / kBN, tm, tn);
-  const int64_t m0 = tm * kBM, n0 = tn * kBN;
+  block_tile((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * BN;
 
-  f32x16 acc[kTM][kTN];
+  f32x16 acc[TM][TN];
 #pragma unroll
-  for (int i = 0; i < kTM; ++i)
+  for (int i = 0; i < TM; ++i)
 #pragma unroll
-    for (int j = 0; j < kTN; ++j)
+    for (int j = 0; j < TN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-  const int64_t kt_count = (K + kBK - 1) / kBK;
-  const Operands op = make_operands(x, w, m0, n0, M, N, K);
+  // Buffer resources over the block's rows of x and W.
+  const int64_t rows_x = (M - m0 < BM) ? M - m0 : BM;
+  const int64_t rows_w = (N - n0 < BN) ? N - n0 : BN;
+  const auto rx = make_rsrc(x + m0 * K, rows_x * K * 2);
+  const auto rw = make_rsrc(w + n0 * K, rows_w * K * 2);
 
-#if LMBP_LIN_DIRECT
-  // Direct path. A stage holds the A tile (BM rows) then the B tile (BN rows), each
-  // row 32 bf16 = four 16-byte units; unit u of row r holds k-chunk u ^ ((r >> 2) & 3),
-  // so that the operand reads of 16 consecutive rows at one k-chunk hit 16 distinct
-  // bank groups. One load instruction of a wave fills 1 KiB (16 rows): lane l writes
-  // unit l % 4 of row l / 4, i.e. fetches k-chunk (l % 4) ^ ((row >> 2) & 3) of that
-  // row (each row's four lanes read its 64 contiguous bytes in permuted order).
-  constexpr int kWaves = kWM * kWN;
-  constexpr int kBlocksA = kBM / 16, kBlocksB = kBN / 16;
-  static_assert(kBlocksA % kWaves == 0 && kBlocksB % kWaves == 0, "load blocks per wave");
-  constexpr int kLA = kBlocksA / kWaves, kLB = kBlocksB / kWaves;
-  constexpr int kLoadsPerStage = kLA + kLB;
-  typedef __attribute__((address_space(3))) void lds_void;
-  uint32_t ld_a[kLA], ld_b[kLB];  // byte offset in the operand (row start + chunk), k step 0
-  {
-    const int r_in = lane >> 2;
-    const int kc = (lane & 3) ^ ((r_in >> 2) & 3);   // block rows start at multiples of 16
+  // Loads: lane l of the wave's q-th 1 KiB block (rows 16 (wave + waves q) + l / 4)
+  // fetches k-chunk kc = (l % 4) ^ ((l / 16) & 3) of its row.
+  const int r_in = lane >> 2;
+  const int kc = (lane & 3) ^ ((r_in >> 2) & 3);
+  uint32_t ld_a[C::kLA], ld_b[C::kLB];  // byte offset of the chunk at K step 0
 #pragma unroll
-    for (int q = 0; q < kLA; ++q)
-      ld_a[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+  for (int q = 0; q < C::kLA; ++q)
+    ld_a[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
 #pragma unroll
-    for (int q = 0; q < kLB; ++q)
-      ld_b[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
-  }
-  const uint32_t kc_bytes = uint32_t(((lane & 3) ^ (((lane >> 2) >> 2) & 3)) * 16);
+  for (int q = 0; q < C::kLB; ++q)
+    ld_b[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+  auto stage_ptr = [&](int64_t kt) { return lds + int(kt % kStages) * C::kStageElems; };
   auto issue_stage = [&](int64_t kt) {
-    uint16_t* S = lds + int(kt % kStages) * kDStageElems;
+    uint16_t* S = stage_ptr(kt);
     const uint32_t k0b = uint32_t(kt * kBK * 2);
-    const bool kin = kt * kBK + int64_t(kc_bytes / 2) < K;
+    const bool kin = kt * kBK + kc * 8 < K;
 #pragma unroll
-    for (int q = 0; q < kLA; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          op.x, (lds_void*)(S + (wave + kWaves * q) * 16 * kBK), 16,
-          kin ? ld_a[q] + k0b : kOutOfRange, 0, 0, 0);
+    for (int q = 0; q < C::kLA; ++q)
+      load_lds16(rx, S + (wave + kWaves * q) * 16 * kBK, kin ? ld_a[q] + k0b : kOutOfRange);
 #pragma unroll
-    for (int q = 0; q < kLB; ++q)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(
-          op.w, (lds_void*)(S + kBM * kBK + (wave + kWaves * q) * 16 * kBK), 16,
-          kin ? ld_b[q] + k0b : kOutOfRange, 0, 0, 0);
+    for (int q = 0; q < C::kLB; ++q)
+      load_lds16(rw, S + BM * kBK + (wave + kWaves * q) * 16 * kBK,
+                 kin ? ld_b[q] + k0b : kOutOfRange);
   };
-  // Operand reads: lane l reads row (base + l % 32), k-chunk 2 kk + l / 32.
-  const int swz = ((lane & 31) >> 2) & 3;   // (row >> 2) & 3; wave rows start at multiples of 32
-  int a_row[kTM], b_row[kTN];
-#pragma unroll
-  for (int i = 0; i < kTM; ++i) a_row[i] = (wm * kTM * 32 + i * 32 + (lane & 31)) * kBK;
-#pragma unroll
-  for (int j = 0; j < kTN; ++j) b_row[j] = kBM * kBK + (wn * kTN * 32 + j * 32 + (lane & 31)) * kBK;
-  auto compute = [&](const uint16_t* S) {
-#pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      const int unit = ((2 * kk + (lane >> 5)) ^ swz) * 8;
-      bf16x8 a[kTM], b[kTN];
-#pragma unroll
-      for (int i = 0; i < kTM; ++i) a[i] = *reinterpret_cast<const bf16x8*>(S + a_row[i] + unit);
-#pragma unroll
-      for (int j = 0; j < kTN; ++j) b[j] = *reinterpret_cast<const bf16x8*>(S + b_row[j] + unit);
-#pragma unroll
-      for (int i = 0; i < kTM; ++i)
-#pragma unroll
-        for (int j = 0; j < kTN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-  };
-  // Wait until at most `pending` stages of this wave's loads are outstanding (the
-  // vector-memory counter counts the direct loads; nothing else uses it in the loop).
-  auto wait_stages = [&](int64_t pending) {
-    static_assert(kStages - 2 <= 3, "wait table");
-    if (pending <= 0) asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-    else if (pending == 1) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kLoadsPerStage) : "memory");
-    else if (pending == 2) asm volatile("s_waitcnt vmcnt(%0)" :: "n"(2 * kLoadsPerStage) : "memory");
-    else asm volatile("s_waitcnt vmcnt(%0)" :: "n"(3 * kLoadsPerStage) : "memory");
-  };
-  for (int s = 0; s < kStages - 1; ++s)
-    if (s < kt_count) issue_stage(s);
-  for (int64_t kt = 0; kt < kt_count; ++kt) {
-    const int64_t issued_after = (kt_count - 1 - kt < kStages - 2) ? kt_count - 1 - kt : kStages - 2;
-    wait_stages(issued_after);
-    asm volatile("s_barrier" ::: "memory");   // every wave's loads of step kt are in LDS
-    if (kt + kStages - 1 < kt_count) issue_stage(kt + kStages - 1);   // into step kt - 1's buffer
-    compute(lds + int(kt % kStages) * kDStageElems);
-  }
-  __syncthreads();
-#else
-  // Operand read offsets (in bf16 elements) inside one stage.
-  const int a_off = (wm * kTM * 32 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
-  const int b_off = kAElems + (wn * kTN * 32 + (lane & 31)) * kLdsRow + 8 * (lane >> 5);
 
-  auto compute = [&](const uint16_t* S) {
+  // Operand reads: lane l reads row (base + l % 32), k-chunk 2 kk + l / 32; wave rows
+  // start at multiples of 32, so the row's swizzle is ((l % 32) >> 2) & 3.
+  const int swz = ((lane & 31) >> 2) & 3;
+  int a_row[TM], b_row[TN];
 #pragma unroll
-    for (int kk = 0; kk < kBK / 16; ++kk) {
-      bf16x8 a[kTM], b[kTN];
+  for (int i = 0; i < TM; ++i) a_row[i] = (wm * TM * 32 + i * 32 + (lane & 31)) * kBK;
 #pragma unroll
-      for (int i = 0; i < kTM; ++i)
-        a[i] = *reinterpret_cast<const bf16x8*>(S + a_off + i * 32 * kLdsRow + kk * 16);
+  for (int j = 0; j < TN; ++j) b_row[j] = BM * kBK + (wn * TN * 32 + j * 32 + (lane & 31)) * kBK;
+  bf16x8 fa[2][TM], fb[2][TN];
+  auto read = [&](const uint16_t* S, int kk, int buf) {
+    const int unit = ((2 * kk + (lane >> 5)) ^ swz) * 8;
 #pragma unroll
-      for (int j = 0; j < kTN; ++j)
-        b[j] = *reinterpret_cast<const bf16x8*>(S + b_off + j * 32 * kLdsRow + kk * 16);
+    for (int i = 0; i < TM; ++i) fa[buf][i] = *reinterpret_cast<const bf16x8*>(S + a_row[i] + unit);
 #pragma unroll
-      for (int i = 0; i < kTM; ++i)
-#pragma unroll
-        for (int j = 0; j < kTN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
+    for (int j = 0; j < TN; ++j) fb[buf][j] = *reinterpret_cast<const bf16x8*>(S + b_row[j] + unit);
   };
-  auto stage_ptr = [&](int64_t kt) { return lds + int(kt & 1) * kStageElems; };
+  auto mfmas = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
+  };
 
-#if LMBP_LIN_PREFETCH == 2
-  // Two register stages: the loads of step kt + 2 are issued before the MFMAs of step
-  // kt, so they have two steps of MFMA work to arrive before they are written to LDS.
-  Stage s0, s1;
-  if (kt_count > 0) load_stage(s0, op, K, 0);
-  if (kt_count > 1) load_stage(s1, op, K, kBK);
-  if (kt_count > 0) store_stage(s0, lds, lds + kAElems);
-  __syncthreads();
-  auto step = [&](int64_t kt, Stage& free_regs, Stage& next_regs) {
-    if (kt + 2 < kt_count) load_stage(free_regs, op, K, (kt + 2) * kBK);
-    compute(stage_ptr(kt));
-    if (kt + 1 < kt_count) {
-      uint16_t* D = stage_ptr(kt + 1);
-      store_stage(next_regs, D, D + kAElems);
-    }
-    __syncthreads();
-  };
-  for (int64_t kt = 0; kt < kt_count; kt += 2) {
-    step(kt, s0, s1);
-    if (kt + 1 < kt_count) step(kt + 1, s1, s0);
-  }
-#else
-  // One register stage: the loads of step kt + 1 are in flight during the MFMAs of kt.
-  Stage st;
+  // Loads of steps at or beyond the last one read zeros into buffers that are no longer
+  // needed, so every step sees the same number of loads in flight and the waits are
+  // constants (the vector-memory counter counts only these loads in the loop).
+  constexpr int kPendingFirst = (kStages - 1) * C::kLoadsPerStage;    // loads after step 0
+  constexpr int kPendingSteady = (kStages - 2) * C::kLoadsPerStage;   // after step kt + 1
+  const int64_t kt_count = (K + kBK - 1) / kBK;
   if (kt_count > 0) {
-    load_stage(st, op, K, 0);
-    store_stage(st, lds, lds + kAElems);
-  }
-  __syncthreads();
-  for (int64_t kt = 0; kt < kt_count; ++kt) {
-    const bool more = kt + 1 < kt_count;
-    if (more) load_stage(st, op, K, (kt + 1) * kBK);
-    compute(stage_ptr(kt));
-    if (more) {
-      uint16_t* D = stage_ptr(kt + 1);
-      store_stage(st, D, D + kAElems);
+#pragma unroll
+    for (int s = 0; s < kStages; ++s) issue_stage(s);
+    asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kPendingFirst) : "memory");
+    asm volatile("s_barrier" ::: "memory");
+    read(stage_ptr(0), 0, 0);
+    for (int64_t kt = 0; kt + 1 < kt_count; ++kt) {
+      const uint16_t* S = stage_ptr(kt);
+#pragma unroll
+      for (int kk = 0; kk < kSlices; ++kk) {
+        if (kk + 1 < kSlices) {
+          read(S, kk + 1, (kk + 1) & 1);
+        } else {
+          // This wave's reads of step kt are complete once their data has arrived; after
+          // the barrier every wave's are, and step kt + 1 is in LDS.
+          asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+          asm volatile("s_waitcnt vmcnt(%0)" :: "n"(kPendingSteady) : "memory");
+          asm volatile("s_barrier" ::: "memory");
+          issue_stage(kt + kStages);   // into step kt's buffer
+          read(stage_ptr(kt + 1), 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the MFMAs
+        mfmas(kk & 1);
+      }
     }
-    __syncthreads();
+    const uint16_t* S = stage_ptr(kt_count - 1);
+#pragma unroll
+    for (int kk = 0; kk < kSlices; ++kk) {
+      if (kk + 1 < kSlices) read(S, kk + 1, (kk + 1) & 1);
+      __builtin_amdgcn_sched_barrier(0);
+      mfmas(kk & 1);
+    }
   }
-#endif
-#endif  // LMBP_LIN_DIRECT
+  __syncthreads();   // waits for every load (including the zero-filling ones) and read
 
   // Epilogue, part 1: bias, rounding to bf16, the tile into LDS (row-major, padded).
   uint16_t* E = lds;
 #pragma unroll
-  for (int j = 0; j < kTN; ++j) {
-    const int col = wn * kTN * 32 + j * 32 + (lane & 31);
+  for (int j = 0; j < TN; ++j) {
+    const int col = wn * TN * 32 + j * 32 + (lane & 31);
     const float bj = (bias != nullptr && n0 + col < N)
                          ? __uint_as_float(uint32_t(bias[n0 + col]) << 16) : 0.0f;
 #pragma unroll
-    for (int i = 0; i < kTM; ++i)
+    for (int i = 0; i < TM; ++i)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = wm * kTM * 32 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        E[row * kEpiRow + col] = uint16_t(pack_bf16x2(acc[i][j][r] + bj, 0.0f) & 0xffffu);
+        const int row = wm * TM * 32 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+        E[row * C::kEpiRow + col] = uint16_t(pack_bf16x2(acc[i][j][r] + bj, 0.0f) & 0xffffu);
       }
   }
   __syncthreads();
 
   // Part 2: thread owns columns c16 .. c16 + 15 of rows tid / (BN/16) + step * g.
-  const int c16 = (tid % kEpiThreadsPerRow) * 16;
+  const int c16 = (tid % C::kEpiThreadsPerRow) * 16;
   if (n0 + c16 >= N) return;  // N is a multiple of 16: a group is wholly in or out
-#pragma unroll 2
-  for (int row = tid / kEpiThreadsPerRow; row < kBM; row += kEpiRowStep) {
+  for (int row = tid / C::kEpiThreadsPerRow; row < BM; row += C::kEpiRowStep) {
     if (m0 + row >= M) break;
-    const u32x4 v0 = *reinterpret_cast<const u32x4*>(E + row * kEpiRow + c16);
-    const u32x4 v1 = *reinterpret_cast<const u32x4*>(E + row * kEpiRow + c16 + 8);
+    const u32x4 v0 = *reinterpret_cast<const u32x4*>(E + row * C::kEpiRow + c16);
+    const u32x4 v1 = *reinterpret_cast<const u32x4*>(E + row * C::kEpiRow + c16 + 8);
     float f0[8], f1[8], o0[8], o1[8];
     BF16::unpack(v0, f0);
     BF16::unpack(v1, f1);
@@ -396,32 +277,54 @@ __global__ __launch_bounds__(kThreads) void linear_act_fwd_kernel(
   }
 }
 
-}  // namespace
+template <class C, int ACT>
+hipError_t launch_tile(int64_t M, int64_t N, int64_t K, const uint16_t* x, const uint16_t* w,
+                       const uint16_t* bias, uint16_t* y, uint32_t* codes, uint16_t* z,
+                       hipStream_t s) {
+  const int64_t blocks = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+  const size_t lds = size_t(C::kLdsElems) * 2;
+  // More than 64 KiB of dynamic LDS must be allowed explicitly (once per kernel).
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(linear_act_fwd_kernel<C, ACT>),
+      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+  if (attr != hipSuccess) return attr;
+  hipLaunchKernelGGL((linear_act_fwd_kernel<C, ACT>), dim3(unsigned(blocks)), dim3(C::kThreads),
+                     lds, s, x, w, bias, y, codes, z, M, N, K);
+  return hipGetLastError();
+}
+
+#ifndef LMBP_LIN_BIG_MIN_ROUNDS
+// Use the 256 x 256 tiles when they fill at least this many rounds of the GPU's CUs
+// (one block per CU); otherwise the 128 x 128 tiles (two blocks per CU) waste less of the
+// last round. Measured: the ViT-B MLP projection (2.3 rounds) runs faster with the small
+// tiles, the LLaMA-7B gate projection (5.4 rounds) with the large ones.
+#define LMBP_LIN_BIG_MIN_ROUNDS 4
+#endif
+
+}  // namespace lin
 
 hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const void* x,
                                  const void* w, const void* bias, void* y, uint32_t* codes,
                                  void* z, hipStream_t s) {
-  const int64_t blocks = ((M + kBM - 1) / kBM) * ((N + kBN - 1) / kBN);
-  if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   auto* xp = static_cast<const uint16_t*>(x);
   auto* wp = static_cast<const uint16_t*>(w);
   auto* bp = static_cast<const uint16_t*>(bias);
   auto* yp = static_cast<uint16_t*>(y);
   auto* zp = static_cast<uint16_t*>(z);
-  const size_t lds = size_t(kLdsElems) * 2;
-  auto kern = act == kGelu ? linear_act_fwd_kernel<kGelu> : linear_act_fwd_kernel<kSilu>;
-  // More than 64 KiB of dynamic LDS must be allowed explicitly (once per kernel).
-  static hipError_t attr_gelu = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(linear_act_fwd_kernel<kGelu>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-  static hipError_t attr_silu = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(linear_act_fwd_kernel<kSilu>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-  const hipError_t attr = act == kGelu ? attr_gelu : attr_silu;
-  if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(kern, dim3(unsigned(blocks)), dim3(kThreads), lds, s, xp, wp, bp, yp, codes,
-                     zp, M, N, K);
-  return hipGetLastError();
+  int device = 0, cus = 256;
+  if (hipGetDevice(&device) == hipSuccess)
+    (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
+  const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
+  const bool big = big_tiles >= int64_t(LMBP_LIN_BIG_MIN_ROUNDS) * cus;
+  using lin::BigTile;
+  using lin::SmallTile;
+  using lin::launch_tile;
+  if (act == kGelu)
+    return big ? launch_tile<BigTile, kGelu>(M, N, K, xp, wp, bp, yp, codes, zp, s)
+               : launch_tile<SmallTile, kGelu>(M, N, K, xp, wp, bp, yp, codes, zp, s);
+  return big ? launch_tile<BigTile, kSilu>(M, N, K, xp, wp, bp, yp, codes, zp, s)
+             : launch_tile<SmallTile, kSilu>(M, N, K, xp, wp, bp, yp, codes, zp, s);
 }
 
 }  // namespace lmbp

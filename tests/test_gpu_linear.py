@@ -73,6 +73,27 @@ def test_exact(m, n, k, act):
 
 
 @pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_exact_large_tiles_ragged(act):
+    """A problem large enough for the 256 x 256 tile configuration (at least four rounds of
+    tiles), ragged in every dimension (m % 256 = 64, n % 256 = 16, k % 32 = 8); exact
+    dyadic arithmetic, compared on sampled rows that include the ragged last tile row."""
+    m, n, k = 8000, 8208, 520
+    print(f"[linear] exact large tiles: m={m} n={n} k={k} act={act}", flush=True)
+    x = inputs.dyadic((m, k), -3, tensor_id=inputs.LIN_X, block=1)
+    w = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_W, block=1)
+    b = inputs.dyadic((n,), -7, tensor_id=inputs.LIN_B, block=1)
+    y, codes, z = run(x, w, b, act)
+    rows = np.unique(np.concatenate([[0, 255, 256, 7935, 7936, 7999],
+                                     np.random.default_rng(3).integers(0, m, 24)]))
+    _, z_s, y_o, c_o = oracle.linear_act_fwd(x[rows], w, b, act)
+    assert np.array_equal(z.reshape(m, n)[rows], z_s), "stored z differs from the exact rounding"
+    got = oracle.unpack_codes(codes, m * n).reshape(m, n)[rows]
+    ref = oracle.unpack_codes(c_o, len(rows) * n).reshape(len(rows), n)
+    assert np.array_equal(got, ref), "codes differ"
+    assert_rel(oracle.decode(y.reshape(m, n)[rows], "bf16"), y_o, 1e-2, "large-tile y (strict)")
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
 def test_exact_no_bias(act):
     check_exact(96, 160, 136, act, bias=False, label="no bias")
 
