@@ -227,6 +227,9 @@ LINEAR_SHAPES = {
 }
 
 
+LINEAR_GLU_SHAPE = (4 * 2048, 11008, 4096)   # LLaMA-7B MLP: x [m, k], gate and up [n, k]
+
+
 def linear_report(torch, lmbp, inputs, dev, reps):
     """Fused linear + ReGELU2 / ReSiLU2 forward against the unfused sequence (library
     GEMM through torch, i.e. hipBLASLt, writing z, then the activation kernel reading
@@ -296,6 +299,38 @@ def linear_report(torch, lmbp, inputs, dev, reps):
               file=sys.stderr, flush=True)
         del x, w, b, y, z, codes
         torch.cuda.empty_cache()
+
+    # The gated form on the LLaMA-7B MLP: gate and up projections + ReSiLU2 inside SwiGLU.
+    m, n, k = LINEAR_GLU_SHAPE
+    name = "llama7b_mlp_swiglu_bf16"
+    T = lambda a: inputs.storage_to_torch(a, dev)
+    x = T(inputs.normal((m, k), 1.0, "bf16", tensor_id=inputs.LIN_X))
+    wg = T(inputs.normal((n, k), k ** -0.5 * 2.0, "bf16", tensor_id=inputs.LIN_W))
+    wu = T(inputs.normal((n, k), k ** -0.5, "bf16", tensor_id=inputs.LIN_B))
+    h, s, u, g = (torch.empty((m, n), dtype=torch.bfloat16, device=dev) for _ in range(4))
+    codes = torch.empty(lmbp.codes_words(m * n), dtype=torch.int32, device=dev)
+    wgt, wut = wg.t(), wu.t()
+
+    def unfused():
+        torch.matmul(x, wgt, out=g)
+        torch.matmul(x, wut, out=u)
+        lmbp.reswiglu2_fwd(g, u, h=h, s=s, codes=codes)
+
+    t_fused, t_unfused = timed_all([
+        lambda: lmbp.linear_swiglu_fwd(x, wg, wu, h=h, s=s, u=u, codes=codes), unfused])
+    flops = 4.0 * m * n * k
+    tf = flops / (t_fused * 1e-6) / 1e12
+    out[name] = {
+        "m": m, "n": n, "k": k, "act": "silu (SwiGLU)", "bias": False,
+        "fused_us": round(t_fused, 1), "fused_TFLOPs": round(tf, 1),
+        "unfused_us": round(t_unfused, 1),
+        "speedup_vs_unfused": round(t_unfused / t_fused, 3),
+        "hbm_bytes_saved": 3 * 2 * m * n,   # g written and read, u read back by the activation
+        "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+    }
+    print(f"[bench] linear {name}: fused {t_fused:.1f} us ({tf:.0f} TFLOP/s), unfused "
+          f"{t_unfused:.1f} us (two library GEMMs + SwiGLU activation)", file=sys.stderr, flush=True)
     return out
 
 

@@ -12,6 +12,7 @@
  *   stepact_fwd / stepact_bwd      k-bit family members with runtime tables (ReGELU2-d, ...)
  *   linear_act_fwd                 a linear layer whose output goes through ReGELU2 /
  *                                  ReSiLU2, fused (the pre-activation stays on chip)
+ *   linear_swiglu_fwd              the LLaMA MLP's two projections + SwiGLU, fused
  *
  * Conventions shared by every call
  * --------------------------------
@@ -196,6 +197,25 @@ lmbp_status msrms_bwd(lmbp_dtype dt, int64_t rows, int64_t cols, const void *dz,
 lmbp_status linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
                            const void *x, const void *w, const void *bias, void *y,
                            uint32_t *codes, void *z, void *stream);
+
+/* ------------------------------------------------------------------------
+ * The gated form of the same fusion, for the LLaMA MLP (Sec. 6; ReSiLU2 inside
+ * SwiGLU as in reswiglu2_fwd): both projections of the MLP's input and the SwiGLU
+ * product in one kernel, the gate pre-activation g never written out.
+ *
+ *   g = bf16( x Wg^T ),  u = bf16( x Wu^T )   (fp32 accumulation, one rounding each)
+ *   h = SiLU(g) * u,  s = SiLU(g),  codes of g — exactly what reswiglu2_fwd computes
+ *   from stored g and u (same bytes); u is written too, since the backward needs it.
+ *
+ *   dt : LMBP_BF16 only. m, n, k, alignment and limits as for linear_act_fwd.
+ *   x [m x k]; w_gate, w_up [n x k]; h, s, u [m x n]; codes of the m x n output;
+ *   g : NULL (not stored) or m x n.
+ * Outputs must not overlap each other or any input. Backward: reswiglu2_bwd on
+ * (dh, u, s, codes), then the two linear layers' products.
+ * ------------------------------------------------------------------------ */
+lmbp_status linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, const void *x,
+                              const void *w_gate, const void *w_up, void *h, void *s, void *u,
+                              uint32_t *codes, void *g, void *stream);
 
 /* ------------------------------------------------------------------------
  * Measurement utility (not part of the method): copies `bytes` bytes from src

@@ -12,7 +12,7 @@ then the activation oracle of ``activations``.
 
 import numpy as np
 
-from .activations import regelu2_fwd, resilu2_fwd
+from .activations import regelu2_fwd, resilu2_fwd, reswiglu2_fwd
 from .dtypes import decode, encode
 
 
@@ -35,3 +35,15 @@ def linear_act_fwd(x_bf16, w_bf16, b_bf16, act):
     fwd = {"gelu": regelu2_fwd, "silu": resilu2_fwd}[act]
     y, codes = fwd(decode(z_s, "bf16"))
     return z, z_s, y, codes
+
+
+def linear_swiglu_fwd(x_bf16, wg_bf16, wu_bf16):
+    """The gated form (the LLaMA MLP's input side, Sec. 6): g = x Wg^T and u = x Wu^T,
+    each rounded once to bf16, then ReSiLU2 inside SwiGLU on the stored g and u.
+    Returns (g exact, g stored, u exact, u stored, h and s in float64, packed codes of g)."""
+    xd = decode(x_bf16, "bf16")
+    g = linear(xd, decode(wg_bf16, "bf16"))
+    u = linear(xd, decode(wu_bf16, "bf16"))
+    g_s, u_s = encode(g, "bf16"), encode(u, "bf16")
+    h, s, codes = reswiglu2_fwd(decode(g_s, "bf16"), decode(u_s, "bf16"))
+    return g, g_s, u, u_s, h, s, codes

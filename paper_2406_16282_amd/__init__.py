@@ -19,6 +19,7 @@ from .binding import (  # noqa: F401
     copy_bytes,
     lib,
     linear_act_fwd,
+    linear_swiglu_fwd,
     msln_bwd,
     msln_fwd,
     msrms_bwd,

@@ -23,7 +23,7 @@ ACT_OPS = ("regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd")
 NORM_OPS = ("msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd")
 GLU_OPS = ("reswiglu2_fwd", "reswiglu2_bwd")
 STEP_OPS = ("stepact_fwd", "stepact_bwd")
-LINEAR_OPS = ("linear_act_fwd",)
+LINEAR_OPS = ("linear_act_fwd", "linear_swiglu_fwd")
 ACT_GELU, ACT_SILU = 0, 1
 
 
@@ -78,6 +78,8 @@ def lib():
     L.stepact_bwd.restype = i32
     L.linear_act_fwd.argtypes = [i32, i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp]
     L.linear_act_fwd.restype = i32
+    L.linear_swiglu_fwd.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.linear_swiglu_fwd.restype = i32
     L.lmbp_copy.argtypes = [vp, vp, i64, vp]
     L.lmbp_copy.restype = i32
     _lib = L
@@ -380,3 +382,36 @@ def linear_act_fwd(x, w, bias=None, act="gelu", y=None, codes=None, z=None, stor
                                               _ptr(y), _ptr(codes),
                                               _ptr(z) if z is not None else None, _stream(x, stream)))
     return (y, codes, z) if z is not None else (y, codes)
+
+
+def linear_swiglu_fwd(x, w_gate, w_up, h=None, s=None, u=None, codes=None, g=None, store_g=False,
+                      stream=None):
+    """Fused LLaMA MLP input side (bf16): g = bf16(x Wg^T), u = bf16(x Wu^T),
+    h = SiLU(g) * u, s = SiLU(g), codes of g. Returns (h, s, u, codes) or, with store_g
+    (or a g tensor given), (h, s, u, codes, g)."""
+    for t, nm in ((x, "x"), (w_gate, "w_gate"), (w_up, "w_up")):
+        _dev(t, nm)
+        if t.dtype != torch.bfloat16:
+            raise TypeError("linear_swiglu_fwd takes bfloat16 tensors")
+    if w_gate.dim() != 2 or w_gate.shape != w_up.shape or x.shape[-1] != w_gate.shape[1]:
+        raise ValueError("x must be [..., k], w_gate and w_up [n, k]")
+    n, k = w_gate.shape
+    m = math.prod(x.shape[:-1])
+    out_shape = (*x.shape[:-1], n)
+
+    def out(t, name):
+        if t is None:
+            return torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
+        _dev(t, name)
+        if t.dtype != torch.bfloat16 or t.numel() != m * n:
+            raise ValueError(f"{name} must be a bfloat16 tensor of m * n elements")
+        return t
+
+    h, s, u = out(h, "h"), out(s, "s"), out(u, "u")
+    if g is not None or store_g:
+        g = out(g, "g")
+    codes = _codes_out(m * n, x.device, codes)
+    _check("linear_swiglu_fwd", lib().linear_swiglu_fwd(
+        BF16, m, n, k, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(h), _ptr(s), _ptr(u), _ptr(codes),
+        _ptr(g) if g is not None else None, _stream(x, stream)))
+    return (h, s, u, codes, g) if g is not None else (h, s, u, codes)

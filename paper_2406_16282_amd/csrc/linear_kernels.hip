@@ -44,6 +44,8 @@
 #include "act_math.hpp"
 #include "lmbp_launch.hpp"
 
+#include <atomic>
+
 namespace lmbp {
 namespace lin {
 
@@ -81,8 +83,11 @@ struct Tile {
   static_assert((kStages - 1) * kLoadsPerStage <= 63, "vector-memory counter range");
 };
 
+#ifndef LMBP_LIN_SMALL
+#define LMBP_LIN_SMALL 128, 128, 2, 2   // BM, BN, WM, WN of the small configuration
+#endif
 using BigTile = Tile<256, 256, 2, 4>;
-using SmallTile = Tile<128, 128, 2, 2>;
+using SmallTile = Tile<LMBP_LIN_SMALL>;
 
 // The target builtins below are wrapped in device functions: used directly in the body of
 // a kernel template, they make the host-side instantiation fail silently and the launch
@@ -113,13 +118,32 @@ __device__ inline void block_tile(int64_t tiles_m, int64_t tiles_n, int64_t& tm,
   tn = r / gsize;
 }
 
-template <class C, int ACT>
-__global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
-    const uint16_t* __restrict__ x, const uint16_t* __restrict__ w,
-    const uint16_t* __restrict__ bias, uint16_t* __restrict__ y, uint32_t* __restrict__ codes,
-    uint16_t* __restrict__ z, int64_t M, int64_t N, int64_t K) {
+// Arguments of the kernel (by value). Plain form: y = act(z), z = x w^T + bias.
+// Gated form (GLU): g = x w^T and u = x w2^T (no bias), y = h = act(g) * u, s = act(g),
+// u stored; z (optional) receives g; codes are those of g.
+struct LinArgs {
+  const uint16_t* x;
+  const uint16_t* w;
+  const uint16_t* w2;
+  const uint16_t* bias;
+  uint16_t* y;
+  uint16_t* s;
+  uint16_t* u;
+  uint32_t* codes;
+  uint16_t* z;
+  int64_t M, N, K;
+};
+
+template <class C, int ACT, bool GLU>
+__global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) {
   using A = ActOf<ACT>;
   constexpr int BM = C::BM, BN = C::BN, TM = C::TM, TN = C::TN, kWaves = C::kWaves;
+  // Output columns per block: the gated form spends half of the B tile on each weight.
+  constexpr int kOut = GLU ? BN / 2 : BN;
+  static_assert(!GLU || C::kLB % 2 == 0, "gated form: each weight fills half the B loads");
+  const uint16_t* __restrict__ x = a.x;
+  const uint16_t* __restrict__ w = a.w;
+  const int64_t M = a.M, N = a.N, K = a.K;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
@@ -127,8 +151,8 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
   const int wm = wave / C::WN, wn = wave % C::WN;
 
   int64_t tm, tn;
-  block_tile((M + BM - 1) / BM, (N + BN - 1) / BN, tm, tn);
-  const int64_t m0 = tm * BM, n0 = tn * BN;
+  block_tile((M + BM - 1) / BM, (N + kOut - 1) / kOut, tm, tn);
+  const int64_t m0 = tm * BM, n0 = tn * kOut;
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -140,9 +164,10 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
 
   // Buffer resources over the block's rows of x and W.
   const int64_t rows_x = (M - m0 < BM) ? M - m0 : BM;
-  const int64_t rows_w = (N - n0 < BN) ? N - n0 : BN;
+  const int64_t rows_w = (N - n0 < kOut) ? N - n0 : kOut;
   const auto rx = make_rsrc(x + m0 * K, rows_x * K * 2);
   const auto rw = make_rsrc(w + n0 * K, rows_w * K * 2);
+  const auto rw2 = make_rsrc(GLU ? a.w2 + n0 * K : w, GLU ? rows_w * K * 2 : 0);
 
   // Loads: lane l of the wave's q-th 1 KiB block (rows 16 (wave + waves q) + l / 4)
   // fetches k-chunk kc = (l % 4) ^ ((l / 16) & 3) of its row.
@@ -152,9 +177,13 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
 #pragma unroll
   for (int q = 0; q < C::kLA; ++q)
     ld_a[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+  // Gated form: B-tile rows below BN / 2 come from w, the others (the second half of the
+  // loads, q >= kLB / 2) from w2, each at its own row offset.
 #pragma unroll
-  for (int q = 0; q < C::kLB; ++q)
-    ld_b[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+  for (int q = 0; q < C::kLB; ++q) {
+    const int row = (wave + kWaves * q) * 16 + r_in - ((GLU && q >= C::kLB / 2) ? BN / 2 : 0);
+    ld_b[q] = uint32_t(row * K * 2 + kc * 16);
+  }
   auto stage_ptr = [&](int64_t kt) { return lds + int(kt % kStages) * C::kStageElems; };
   auto issue_stage = [&](int64_t kt) {
     uint16_t* S = stage_ptr(kt);
@@ -165,7 +194,7 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
       load_lds16(rx, S + (wave + kWaves * q) * 16 * kBK, kin ? ld_a[q] + k0b : kOutOfRange);
 #pragma unroll
     for (int q = 0; q < C::kLB; ++q)
-      load_lds16(rw, S + BM * kBK + (wave + kWaves * q) * 16 * kBK,
+      load_lds16((GLU && q >= C::kLB / 2) ? rw2 : rw, S + BM * kBK + (wave + kWaves * q) * 16 * kBK,
                  kin ? ld_b[q] + k0b : kOutOfRange);
   };
 
@@ -235,12 +264,13 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
   __syncthreads();   // waits for every load (including the zero-filling ones) and read
 
   // Epilogue, part 1: bias, rounding to bf16, the tile into LDS (row-major, padded).
+  // Gated form: columns [0, BN/2) hold g, [BN/2, BN) hold u of the same output columns.
   uint16_t* E = lds;
 #pragma unroll
   for (int j = 0; j < TN; ++j) {
     const int col = wn * TN * 32 + j * 32 + (lane & 31);
-    const float bj = (bias != nullptr && n0 + col < N)
-                         ? __uint_as_float(uint32_t(bias[n0 + col]) << 16) : 0.0f;
+    const float bj = (!GLU && a.bias != nullptr && n0 + col < N)
+                         ? __uint_as_float(uint32_t(a.bias[n0 + col]) << 16) : 0.0f;
 #pragma unroll
     for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -251,10 +281,12 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
   }
   __syncthreads();
 
-  // Part 2: thread owns columns c16 .. c16 + 15 of rows tid / (BN/16) + step * g.
-  const int c16 = (tid % C::kEpiThreadsPerRow) * 16;
+  // Part 2: thread owns output columns c16 .. c16 + 15 of rows tid / (kOut/16) + step * g.
+  constexpr int kTpr = kOut / 16;
+  static_assert(C::kThreads % kTpr == 0, "epilogue mapping");
+  const int c16 = (tid % kTpr) * 16;
   if (n0 + c16 >= N) return;  // N is a multiple of 16: a group is wholly in or out
-  for (int row = tid / C::kEpiThreadsPerRow; row < BM; row += C::kEpiRowStep) {
+  for (int row = tid / kTpr; row < BM; row += C::kThreads / kTpr) {
     if (m0 + row >= M) break;
     const u32x4 v0 = *reinterpret_cast<const u32x4*>(E + row * C::kEpiRow + c16);
     const u32x4 v1 = *reinterpret_cast<const u32x4*>(E + row * C::kEpiRow + c16 + 8);
@@ -267,30 +299,58 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(
       o1[e] = act_value<ACT, false>(f1[e]);
     }
     const int64_t base = (m0 + row) * N + n0 + c16;   // flat element index, multiple of 16
-    *reinterpret_cast<u32x4*>(y + base) = BF16::pack(o0);
-    *reinterpret_cast<u32x4*>(y + base + 8) = BF16::pack(o1);
-    codes[base / 16] = codes_of<A>(f0) | (codes_of<A>(f1) << 16);
-    if (z != nullptr) {
-      *reinterpret_cast<u32x4*>(z + base) = v0;
-      *reinterpret_cast<u32x4*>(z + base + 8) = v1;
+    if constexpr (GLU) {
+      // Same arithmetic as the SwiGLU activation kernel on stored g and u.
+      const u32x4 u0 = *reinterpret_cast<const u32x4*>(E + row * C::kEpiRow + BN / 2 + c16);
+      const u32x4 u1 = *reinterpret_cast<const u32x4*>(E + row * C::kEpiRow + BN / 2 + c16 + 8);
+      float g0[8], g1[8];
+      BF16::unpack(u0, g0);
+      BF16::unpack(u1, g1);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        g0[e] = o0[e] * g0[e];
+        g1[e] = o1[e] * g1[e];
+      }
+      *reinterpret_cast<u32x4*>(a.y + base) = BF16::pack(g0);
+      *reinterpret_cast<u32x4*>(a.y + base + 8) = BF16::pack(g1);
+      *reinterpret_cast<u32x4*>(a.s + base) = BF16::pack(o0);
+      *reinterpret_cast<u32x4*>(a.s + base + 8) = BF16::pack(o1);
+      *reinterpret_cast<u32x4*>(a.u + base) = u0;
+      *reinterpret_cast<u32x4*>(a.u + base + 8) = u1;
+    } else {
+      *reinterpret_cast<u32x4*>(a.y + base) = BF16::pack(o0);
+      *reinterpret_cast<u32x4*>(a.y + base + 8) = BF16::pack(o1);
+    }
+    a.codes[base / 16] = codes_of<A>(f0) | (codes_of<A>(f1) << 16);
+    if (a.z != nullptr) {
+      *reinterpret_cast<u32x4*>(a.z + base) = v0;
+      *reinterpret_cast<u32x4*>(a.z + base + 8) = v1;
     }
   }
 }
 
-template <class C, int ACT>
-hipError_t launch_tile(int64_t M, int64_t N, int64_t K, const uint16_t* x, const uint16_t* w,
-                       const uint16_t* bias, uint16_t* y, uint32_t* codes, uint16_t* z,
-                       hipStream_t s) {
-  const int64_t blocks = ((M + C::BM - 1) / C::BM) * ((N + C::BN - 1) / C::BN);
+template <class C, int ACT, bool GLU>
+hipError_t launch_tile(const LinArgs& a, hipStream_t s) {
+  constexpr int kOut = GLU ? C::BN / 2 : C::BN;
+  const int64_t blocks = ((a.M + C::BM - 1) / C::BM) * ((a.N + kOut - 1) / kOut);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   const size_t lds = size_t(C::kLdsElems) * 2;
-  // More than 64 KiB of dynamic LDS must be allowed explicitly (once per kernel).
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(linear_act_fwd_kernel<C, ACT>),
-      hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
-  if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL((linear_act_fwd_kernel<C, ACT>), dim3(unsigned(blocks)), dim3(C::kThreads),
-                     lds, s, x, w, bias, y, codes, z, M, N, K);
+  // More than 64 KiB of dynamic LDS must be allowed explicitly, per kernel and device;
+  // the attribute is set on the first launch on each device.
+  constexpr int kMaxDevices = 64;
+  static std::atomic<bool> attr_set[kMaxDevices];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  if (!attr_set[dev].load(std::memory_order_acquire)) {
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(linear_act_fwd_kernel<C, ACT, GLU>),
+                            hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
+    if (e != hipSuccess) return e;
+    attr_set[dev].store(true, std::memory_order_release);
+  }
+  hipLaunchKernelGGL((linear_act_fwd_kernel<C, ACT, GLU>), dim3(unsigned(blocks)),
+                     dim3(C::kThreads), lds, s, a);
   return hipGetLastError();
 }
 
@@ -304,27 +364,43 @@ hipError_t launch_tile(int64_t M, int64_t N, int64_t K, const uint16_t* x, const
 
 }  // namespace lin
 
-hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const void* x,
-                                 const void* w, const void* bias, void* y, uint32_t* codes,
-                                 void* z, hipStream_t s) {
-  auto* xp = static_cast<const uint16_t*>(x);
-  auto* wp = static_cast<const uint16_t*>(w);
-  auto* bp = static_cast<const uint16_t*>(bias);
-  auto* yp = static_cast<uint16_t*>(y);
-  auto* zp = static_cast<uint16_t*>(z);
+namespace {
+// Large tiles when they fill at least LMBP_LIN_BIG_MIN_ROUNDS rounds of the CUs.
+bool use_big_tiles(int64_t M, int64_t N_tile_cols) {
   int device = 0, cus = 256;
   if (hipGetDevice(&device) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
-  const int64_t big_tiles = ((M + 255) / 256) * ((N + 255) / 256);
-  const bool big = big_tiles >= int64_t(LMBP_LIN_BIG_MIN_ROUNDS) * cus;
+  const int64_t big_tiles = ((M + 255) / 256) * ((N_tile_cols + 255) / 256);
+  return big_tiles >= int64_t(LMBP_LIN_BIG_MIN_ROUNDS) * cus;
+}
+}  // namespace
+
+hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const void* x,
+                                 const void* w, const void* bias, void* y, uint32_t* codes,
+                                 void* z, hipStream_t s) {
+  lin::LinArgs a{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), nullptr,
+                 static_cast<const uint16_t*>(bias), static_cast<uint16_t*>(y), nullptr,
+                 nullptr, codes, static_cast<uint16_t*>(z), M, N, K};
+  const bool big = use_big_tiles(M, N);
   using lin::BigTile;
   using lin::SmallTile;
   using lin::launch_tile;
   if (act == kGelu)
-    return big ? launch_tile<BigTile, kGelu>(M, N, K, xp, wp, bp, yp, codes, zp, s)
-               : launch_tile<SmallTile, kGelu>(M, N, K, xp, wp, bp, yp, codes, zp, s);
-  return big ? launch_tile<BigTile, kSilu>(M, N, K, xp, wp, bp, yp, codes, zp, s)
-             : launch_tile<SmallTile, kSilu>(M, N, K, xp, wp, bp, yp, codes, zp, s);
+    return big ? launch_tile<BigTile, kGelu, false>(a, s) : launch_tile<SmallTile, kGelu, false>(a, s);
+  return big ? launch_tile<BigTile, kSilu, false>(a, s) : launch_tile<SmallTile, kSilu, false>(a, s);
+}
+
+hipError_t launch_linear_glu_fwd(int64_t M, int64_t N, int64_t K, const void* x, const void* w_gate,
+                                 const void* w_up, void* h, void* s_out, void* u, uint32_t* codes,
+                                 void* g, hipStream_t s) {
+  lin::LinArgs a{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_gate),
+                 static_cast<const uint16_t*>(w_up), nullptr, static_cast<uint16_t*>(h),
+                 static_cast<uint16_t*>(s_out), static_cast<uint16_t*>(u), codes,
+                 static_cast<uint16_t*>(g), M, N, K};
+  // Each block covers half as many output columns as its tile width.
+  const bool big = use_big_tiles(M, 2 * N);
+  return big ? lin::launch_tile<lin::BigTile, kSilu, true>(a, s)
+             : lin::launch_tile<lin::SmallTile, kSilu, true>(a, s);
 }
 
 }  // namespace lmbp

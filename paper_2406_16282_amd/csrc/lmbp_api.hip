@@ -269,6 +269,36 @@ lmbp_status linear_act_fwd_impl(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t 
                                               static_cast<hipStream_t>(stream)));
 }
 
+lmbp_status linear_swiglu_fwd_impl(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, const void* x,
+                                   const void* w_gate, const void* w_up, void* h, void* s, void* u,
+                                   uint32_t* codes, void* g, void* stream) {
+  if (!known_dtype(dt) || dt != LMBP_BF16) return LMBP_EDTYPE;
+  const int64_t lim = int64_t(1) << 31;
+  if (m < 0 || n < 0 || k < 0 || m >= lim || n >= lim || k >= lim) return LMBP_EINVAL;
+  if (n % 16 != 0 || k % 8 != 0 || k > (int64_t(1) << 21)) return LMBP_EINVAL;
+  if (m == 0 || n == 0) return LMBP_OK;
+  if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (!h || !s || !u || !codes || (k > 0 && (!x || !w_gate || !w_up))) return LMBP_EINVAL;
+  const void* sixteen[] = {x, w_gate, w_up, h, s, u, g};
+  for (const void* p : sixteen)
+    if (p && !aligned(p, 16)) return LMBP_EINVAL;
+  if (!aligned(codes, 4)) return LMBP_EINVAL;
+  const uint64_t mn = uint64_t(m) * uint64_t(n);
+  const Span outs[5] = {span(h, mn * 2), span(s, mn * 2), span(u, mn * 2),
+                        span(codes, lmbp_codes_bytes(int64_t(mn))), span(g, g ? mn * 2 : 0)};
+  const Span ins[3] = {span(x, x ? uint64_t(m) * uint64_t(k) * 2 : 0),
+                       span(w_gate, w_gate ? uint64_t(n) * uint64_t(k) * 2 : 0),
+                       span(w_up, w_up ? uint64_t(n) * uint64_t(k) * 2 : 0)};
+  for (int i = 0; i < 5; ++i) {
+    for (int j = i + 1; j < 5; ++j)
+      if (overlaps(outs[i], outs[j])) return LMBP_EOVERLAP;
+    for (const Span& in : ins)
+      if (overlaps(outs[i], in)) return LMBP_EOVERLAP;
+  }
+  return from_hip(lmbp::launch_linear_glu_fwd(m, n, k, x, w_gate, w_up, h, s, u, codes, g,
+                                              static_cast<hipStream_t>(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -347,6 +377,12 @@ lmbp_status linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, in
                            const void* x, const void* w, const void* bias, void* y,
                            uint32_t* codes, void* z, void* stream) {
   return linear_act_fwd_impl(act, dt, m, n, k, x, w, bias, y, codes, z, stream);
+}
+
+lmbp_status linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, const void* x,
+                              const void* w_gate, const void* w_up, void* h, void* s, void* u,
+                              uint32_t* codes, void* g, void* stream) {
+  return linear_swiglu_fwd_impl(dt, m, n, k, x, w_gate, w_up, h, s, u, codes, g, stream);
 }
 
 lmbp_status lmbp_copy(const void* src, void* dst, int64_t bytes, void* stream) {

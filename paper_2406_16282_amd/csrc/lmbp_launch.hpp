@@ -46,6 +46,12 @@ hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const
                                  const void* w, const void* bias, void* y, uint32_t* codes,
                                  void* z, hipStream_t s);
 
+// Gated form: g = bf16(x Wg^T), u = bf16(x Wu^T); h = SiLU(g) * u, s = SiLU(g), u stored,
+// codes of g; g stored when non-null. Same requirements as launch_linear_act_fwd.
+hipError_t launch_linear_glu_fwd(int64_t M, int64_t N, int64_t K, const void* x, const void* w_gate,
+                                 const void* w_up, void* h, void* s_out, void* u, uint32_t* codes,
+                                 void* g, hipStream_t s);
+
 hipError_t launch_copy(const void* src, void* dst, int64_t bytes, hipStream_t s);
 
 }  // namespace lmbp

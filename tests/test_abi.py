@@ -150,6 +150,22 @@ def test_linear_act_errors(L):
     assert f(G, B.BF16, 4, 32, 16, x, w, bias, y, c, bias - 16, None) == B.EOVERLAP
 
 
+def test_linear_swiglu_errors(L):
+    f = L.linear_swiglu_fwd
+    x, wg, wu, h, s, u, c, g = (P + 4096 * i for i in range(8))
+    assert f(B.FP32, 4, 32, 16, x, wg, wu, h, s, u, c, g, None) == B.EDTYPE
+    assert f(B.BF16, -1, 32, 16, x, wg, wu, h, s, u, c, g, None) == B.EINVAL
+    assert f(B.BF16, 4, 24, 16, x, wg, wu, h, s, u, c, g, None) == B.EINVAL      # n % 16
+    assert f(B.BF16, 4, 32, 12, x, wg, wu, h, s, u, c, g, None) == B.EINVAL      # k % 8
+    assert f(B.BF16, 0, 32, 16, x, wg, wu, h, s, u, c, g, None) == B.OK
+    assert f(B.BF16, 4, 32, 16, x, wg, wu, h, None, u, c, g, None) == B.EINVAL
+    assert f(B.BF16, 4, 32, 16, x, None, wu, h, s, u, c, g, None) == B.EINVAL
+    assert f(B.BF16, 4, 32, 16, x, wg, wu + 8, h, s, u, c, g, None) == B.EINVAL   # alignment
+    assert f(B.BF16, 4, 32, 16, x, wg, wu, h, h, u, c, g, None) == B.EOVERLAP     # s on h
+    assert f(B.BF16, 4, 32, 16, x, wg, wu, h, s, wu, c, g, None) == B.EOVERLAP    # u on w_up
+    assert f(B.BF16, 4, 32, 16, x, wg, wu, h, s, u, c, c - 16, None) == B.EOVERLAP  # g on codes
+
+
 def test_copy_errors(L):
     assert L.lmbp_copy(P, P + 4096, -1, None) == B.EINVAL
     assert L.lmbp_copy(P, P + 4096, 0, None) == B.OK

@@ -175,3 +175,52 @@ def test_store_z_does_not_change_outputs_and_matches_the_activation_op():
         y3, c3 = op(T(z1))
         torch.cuda.synchronize()
         assert np.array_equal(H(y3), y1) and np.array_equal(H(c3), c1)
+
+
+def run_glu(x, wg, wu):
+    out = lmbp.linear_swiglu_fwd(T(x), T(wg), T(wu), store_g=True)
+    torch.cuda.synchronize()
+    return tuple(H(t) for t in out)
+
+
+GLU_SHAPES = [
+    (128, 64, 64),        # one small tile (64 output columns), one K step
+    (200, 208, 200),      # several tiles, ragged m, n (n % 64 = 16) and K
+    (8000, 4112, 520),    # large tiles (>= four rounds), ragged in every dimension
+]
+
+
+@pytest.mark.parametrize("m,n,k", GLU_SHAPES)
+def test_swiglu_exact(m, n, k):
+    """Gated form on dyadic inputs: g and u bit-exact, codes bit-exact, h and s within the
+    SwiGLU rules; for the large problem compared on sampled rows."""
+    print(f"[linear] swiglu exact: m={m} n={n} k={k}", flush=True)
+    x = inputs.dyadic((m, k), -3, tensor_id=inputs.LIN_X, block=m + n)
+    wg = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_W, block=m + n)
+    wu = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_B, block=m + n)
+    h, s, u, codes, g = run_glu(x, wg, wu)
+    rows = np.arange(m) if m <= 512 else np.unique(
+        np.concatenate([[0, 255, 256, m - 1], np.random.default_rng(5).integers(0, m, 20)]))
+    _, g_s, _, u_s, h_o, s_o, c_o = oracle.linear_swiglu_fwd(x[rows], wg, wu)
+    assert np.array_equal(g.reshape(m, n)[rows], g_s), "g differs from the exact rounding"
+    assert np.array_equal(u.reshape(m, n)[rows], u_s), "u differs from the exact rounding"
+    got = oracle.unpack_codes(codes, m * n).reshape(m, n)[rows]
+    ref = oracle.unpack_codes(c_o, len(rows) * n).reshape(len(rows), n)
+    assert np.array_equal(got, ref), "codes differ"
+    assert_rel(oracle.decode(s.reshape(m, n)[rows], "bf16"), s_o, 1e-2, "s (strict)")
+    assert_mixed(oracle.decode(h.reshape(m, n)[rows], "bf16"), h_o, 2e-2, "h")
+
+
+def test_swiglu_matches_the_activation_kernel():
+    """h, s and codes are the bytes reswiglu2_fwd produces from the stored g and u."""
+    x = inputs.normal((300, 512), 1.0, "bf16", tensor_id=inputs.LIN_X)
+    wg = inputs.normal((688, 512), 512 ** -0.5 * 2.0, "bf16", tensor_id=inputs.LIN_W)
+    wu = inputs.normal((688, 512), 512 ** -0.5, "bf16", tensor_id=inputs.LIN_B)
+    h, s, u, codes, g = run_glu(x, wg, wu)
+    h2, s2, c2 = lmbp.reswiglu2_fwd(T(g), T(u))
+    torch.cuda.synchronize()
+    assert np.array_equal(H(h2), h) and np.array_equal(H(s2), s) and np.array_equal(H(c2), codes)
+    h3, s3, u3, c3 = (H(t) for t in lmbp.linear_swiglu_fwd(T(x), T(wg), T(wu)))
+    torch.cuda.synchronize()
+    assert np.array_equal(h3, h) and np.array_equal(s3, s) and np.array_equal(u3, u) \
+        and np.array_equal(c3, codes), "storing g must not change the other outputs"

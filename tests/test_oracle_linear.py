@@ -69,3 +69,13 @@ def test_linear_act_rounds_z_once():
     z, z_s, _, _ = oracle.linear_act_fwd(x, w, None, "gelu")
     assert z[0, 0] == 1.0 + 2.0 ** -8 and oracle.decode(z_s, "bf16")[0, 0] == 1.0
     assert oracle.decode(z_s, "bf16")[0, 1] == 1.0 + 2.0 ** -7
+
+
+def test_linear_swiglu_composition():
+    """Wg = Wu = I: g = u = x, and the outputs are the SwiGLU activation oracle's on (x, x)."""
+    x = inputs.normal((4, 32), 2.0, "bf16", tensor_id=inputs.LIN_X)
+    eye = inputs.to_storage(np.eye(32), "bf16")
+    g, g_s, u, u_s, h, s, codes = oracle.linear_swiglu_fwd(x, eye, eye)
+    assert np.array_equal(g_s, x) and np.array_equal(u_s, x)
+    h_ref, s_ref, c_ref = oracle.reswiglu2_fwd(oracle.decode(x, "bf16"), oracle.decode(x, "bf16"))
+    assert np.array_equal(h, h_ref) and np.array_equal(s, s_ref) and np.array_equal(codes, c_ref)
