@@ -11,6 +11,9 @@
   forward fused into one kernel (the pre-activation is never stored); saves x (for the
   weight gradient) and the codes. Backward: dz = dy * slope[code] by the activation
   kernel, then the two products of a linear layer's backward (library GEMMs).
+* ``LinearReSwiGLU2``: the LLaMA MLP's gate and up projections with SwiGLU, forward fused
+  in one kernel (g never stored); backward through the SwiGLU activation backward and
+  the linear layers' products.
 * ``merge_norm_into_linears``: folds a norm's affine (alpha, beta) into the linear layers
   that consume its output, W~ = W diag(alpha), b~ = W beta + b (Sec. 5.2), and returns
   the parameter-free MS norm to use in its place.
@@ -122,6 +125,39 @@ class LinearReGELU2(_LinearActModule):
 class LinearReSiLU2(_LinearActModule):
     """SiLU(x W^T + b) with ReSiLU2's backward (Sec. 4.2), forward fused in one kernel."""
     which = "silu"
+
+
+class _LinearSwiGLU(torch.autograd.Function):
+    @staticmethod
+    def forward(ctx, x, w_gate, w_up):
+        x2 = _flat(x).reshape(-1, x.shape[-1])
+        h, s, u, codes = binding.linear_swiglu_fwd(x2, _flat(w_gate), _flat(w_up))
+        ctx.x_shape = x.shape
+        ctx.save_for_backward(x2, w_gate, w_up, s, u, codes)
+        return h.reshape(*x.shape[:-1], w_gate.shape[0])
+
+    @staticmethod
+    def backward(ctx, dh):
+        x2, w_gate, w_up, s, u, codes = ctx.saved_tensors
+        dg, du = binding.reswiglu2_bwd(_flat(dh).reshape(-1, w_gate.shape[0]), u, s, codes)
+        dx = ((dg @ w_gate) + (du @ w_up)).reshape(ctx.x_shape) if ctx.needs_input_grad[0] else None
+        dwg = (dg.t().contiguous() @ x2) if ctx.needs_input_grad[1] else None
+        dwu = (du.t().contiguous() @ x2) if ctx.needs_input_grad[2] else None
+        return dx, dwg, dwu
+
+
+class LinearReSwiGLU2(nn.Module):
+    """The LLaMA MLP's input side, SiLU(x Wg^T) * (x Wu^T), with ReSiLU2's backward for
+    the SiLU factor; forward fused in one kernel (bf16; out_features a multiple of 16,
+    in_features of 8). Saves x, s = SiLU(g), u and the codes of g."""
+
+    def __init__(self, in_features, out_features, device=None, dtype=torch.bfloat16):
+        super().__init__()
+        self.gate = nn.Linear(in_features, out_features, bias=False, device=device, dtype=dtype)
+        self.up = nn.Linear(in_features, out_features, bias=False, device=device, dtype=dtype)
+
+    def forward(self, x):
+        return _LinearSwiGLU.apply(x, self.gate.weight, self.up.weight)
 
 
 class ReGELU2(nn.Module):

@@ -143,3 +143,33 @@ def test_fused_linear_act_module(which):
     assert_mixed(oracle.decode(H(mod.weight.grad), "bf16"), dz.T @ xd, 2e-2, "fused module dW")
     assert_mixed(oracle.decode(H(mod.bias.grad), "bf16").reshape(1, -1), dz.sum(0).reshape(1, -1),
                  2e-2, "fused module db")
+
+
+
+def test_fused_linear_swiglu_module():
+    """LinearReSwiGLU2 against the oracle: forward h, and the Approx-BP gradients
+    dg = dh * u * slope[code(g)], du = dh * s, dx = dg Wg + du Wu, dWg = dg^T x, dWu = du^T x
+    (fp64 from the oracle's stored g, u). Dyadic inputs keep the GPU's g and u exact."""
+    from paper_2406_16282_amd.nn import LinearReSwiGLU2
+    m, k, n = 96, 64, 80
+    x = inputs.dyadic((m, k), -3, tensor_id=inputs.LIN_X)
+    wg = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_W)
+    wu = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_B)
+    dh = inputs.normal((m, n), 1.0, "bf16", tensor_id=inputs.ACT_DY)
+    mod = LinearReSwiGLU2(k, n, device=DEV)
+    with torch.no_grad():
+        mod.gate.weight.copy_(T(wg))
+        mod.up.weight.copy_(T(wu))
+    xt = T(x, True)
+    h = mod(xt)
+    h.backward(T(dh))
+    _, g_s, _, u_s, h_o, s_o, c_o = oracle.linear_swiglu_fwd(x, wg, wu)
+    assert_mixed(oracle.decode(H(h), "bf16"), h_o, 2e-2, "swiglu module h")
+    s_st = oracle.decode(oracle.encode(s_o, "bf16"), "bf16")
+    dg_o, du_o = oracle.reswiglu2_bwd(oracle.decode(dh, "bf16"), oracle.decode(u_s, "bf16"), s_st, c_o)
+    dg_o = oracle.decode(oracle.encode(dg_o, "bf16"), "bf16")
+    du_o = oracle.decode(oracle.encode(du_o, "bf16"), "bf16")
+    xd, wgd, wud = (oracle.decode(a, "bf16") for a in (x, wg, wu))
+    assert_mixed(oracle.decode(H(xt.grad), "bf16"), dg_o @ wgd + du_o @ wud, 2e-2, "swiglu module dx")
+    assert_mixed(oracle.decode(H(mod.gate.weight.grad), "bf16"), dg_o.T @ xd, 2e-2, "swiglu module dWg")
+    assert_mixed(oracle.decode(H(mod.up.weight.grad), "bf16"), du_o.T @ xd, 2e-2, "swiglu module dWu")
