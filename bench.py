@@ -120,10 +120,21 @@ def cpu_baseline(w, min_seconds=10.0):
         if elapsed >= min_seconds:
             break
     step_bytes = sum(algorithmic_bytes(w).values())
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {
         "value": round(passes * step_bytes / elapsed / 1e9, 4),
         "unit": "GB/s",
         "cores": 1,
+        "host_cpu": model,
+        "host_cpus_visible": os.cpu_count(),
         "kind": "oracle",
         "sample": (f"{passes} full pass(es) of the step (all {w.norm.rows} rows of every tensor), "
                    f"fp64 NumPy, {elapsed:.2f} s wall"),
