@@ -124,6 +124,14 @@ def _dev(t, what):
     return t
 
 
+def _on(t, ref, what):
+    """``t`` must be a GPU tensor on the same device as ``ref``."""
+    _dev(t, what)
+    if t.device != ref.device:
+        raise ValueError(f"{what} must be on {ref.device}, not {t.device}")
+    return t
+
+
 def _stream(t, stream):
     if stream is None:
         return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
@@ -160,18 +168,20 @@ def _act_fwd(op, x, y, codes, stream):
     dt = _dtype_code(x)
     y = _like(x, y, "y")
     codes = _codes_out(x.numel(), x.device, codes)
-    _check(op, getattr(lib(), op)(dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes), _stream(x, stream)))
+    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+        _check(op, getattr(lib(), op)(dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes), _stream(x, stream)))
     return y, codes
 
 
 def _act_bwd(op, dy, codes, dx, stream):
     _dev(dy, "dy")
     dt = _dtype_code(dy)
-    _dev(codes, "codes")
+    _on(codes, dy, "codes")
     if codes.dtype != torch.int32 or codes.numel() < codes_words(dy.numel()):
         raise ValueError("codes must be the int32 buffer written by the forward")
     dx = _like(dy, dx, "dx")
-    _check(op, getattr(lib(), op)(dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx), _stream(dy, stream)))
+    with torch.cuda.device(dy.device):   # launches go to the tensors' GPU
+        _check(op, getattr(lib(), op)(dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx), _stream(dy, stream)))
     return dx
 
 
@@ -210,8 +220,9 @@ def reswiglu2_fwd(g, u, h=None, s=None, codes=None, stream=None):
     h = _like(g, h, "h")
     s = _like(g, s, "s")
     codes = _codes_out(g.numel(), g.device, codes)
-    _check("reswiglu2_fwd", lib().reswiglu2_fwd(dt, g.numel(), _ptr(g), _ptr(u), _ptr(h), _ptr(s),
-                                                _ptr(codes), _stream(g, stream)))
+    with torch.cuda.device(g.device):   # launches go to the tensors' GPU
+        _check("reswiglu2_fwd", lib().reswiglu2_fwd(dt, g.numel(), _ptr(g), _ptr(u), _ptr(h), _ptr(s),
+                                                    _ptr(codes), _stream(g, stream)))
     return h, s, codes
 
 
@@ -221,13 +232,14 @@ def reswiglu2_bwd(dh, u, s, codes, dg=None, du=None, stream=None):
     dt = _dtype_code(dh)
     _same(u, dh, "u")
     _same(s, dh, "s")
-    _dev(codes, "codes")
+    _on(codes, dh, "codes")
     if codes.dtype != torch.int32 or codes.numel() < codes_words(dh.numel()):
         raise ValueError("codes must be the int32 buffer written by the forward")
     dg = _like(dh, dg, "dg")
     du = _like(dh, du, "du")
-    _check("reswiglu2_bwd", lib().reswiglu2_bwd(dt, dh.numel(), _ptr(dh), _ptr(u), _ptr(s), _ptr(codes),
-                                                _ptr(dg), _ptr(du), _stream(dh, stream)))
+    with torch.cuda.device(dh.device):   # launches go to the tensors' GPU
+        _check("reswiglu2_bwd", lib().reswiglu2_bwd(dt, dh.numel(), _ptr(dh), _ptr(u), _ptr(s), _ptr(codes),
+                                                    _ptr(dg), _ptr(du), _stream(dh, stream)))
     return dg, du
 
 
@@ -249,10 +261,11 @@ def stepact_fwd(x, act, thresholds, bits, y=None, codes=None, stream=None):
     words = int(lib().lmbp_stepact_codes_bytes(bits, x.numel())) // 4
     if codes is None:
         codes = torch.empty(words, dtype=torch.int32, device=x.device)
-    elif codes.dtype != torch.int32 or codes.numel() < words or codes.device != x.device:
+    elif _on(codes, x, "codes").dtype != torch.int32 or codes.numel() < words:
         raise ValueError(f"codes must be an int32 GPU tensor of at least {words} words")
-    _check("stepact_fwd", lib().stepact_fwd(a, bits, tab, dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes),
-                                            _stream(x, stream)))
+    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+        _check("stepact_fwd", lib().stepact_fwd(a, bits, tab, dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes),
+                                                _stream(x, stream)))
     return y, codes
 
 
@@ -260,14 +273,15 @@ def stepact_bwd(dy, codes, levels, bits, dx=None, stream=None):
     """Backward of stepact_fwd: dx = dy * levels[code] (2^k levels)."""
     _dev(dy, "dy")
     dt = _dtype_code(dy)
-    _dev(codes, "codes")
+    _on(codes, dy, "codes")
     words = int(lib().lmbp_stepact_codes_bytes(bits, dy.numel())) // 4
     if codes.dtype != torch.int32 or codes.numel() < words:
         raise ValueError("codes must be the int32 buffer written by the forward")
     tab = _doubles(levels, 1 << bits, "levels")
     dx = _like(dy, dx, "dx")
-    _check("stepact_bwd", lib().stepact_bwd(bits, tab, dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx),
-                                            _stream(dy, stream)))
+    with torch.cuda.device(dy.device):   # launches go to the tensors' GPU
+        _check("stepact_bwd", lib().stepact_bwd(bits, tab, dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx),
+                                                _stream(dy, stream)))
     return dx
 
 
@@ -287,18 +301,19 @@ def _norm_fwd(op, x, eps, z, rstd, stream):
     if rstd is None:
         rstd = torch.empty(x.shape[:-1], dtype=torch.float32, device=x.device)
     else:
-        _dev(rstd, "rstd")
+        _on(rstd, x, "rstd")
         if rstd.dtype != torch.float32 or rstd.numel() != rows:
             raise ValueError("rstd must be float32 with one value per row")
-    _check(op, getattr(lib(), op)(dt, rows, cols, float(eps), _ptr(x), _ptr(z), _ptr(rstd),
-                                  _stream(x, stream)))
+    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+        _check(op, getattr(lib(), op)(dt, rows, cols, float(eps), _ptr(x), _ptr(z), _ptr(rstd),
+                                      _stream(x, stream)))
     return z, rstd
 
 
 def _norm_bwd(op, dz, z, rstd, dx, stream):
     _dev(dz, "dz")
-    _dev(z, "z")
-    _dev(rstd, "rstd")
+    _on(z, dz, "z")
+    _on(rstd, dz, "rstd")
     dt = _dtype_code(dz)
     if z.dtype != dz.dtype or z.shape != dz.shape:
         raise ValueError("z must match dz in dtype and shape")
@@ -306,8 +321,9 @@ def _norm_bwd(op, dz, z, rstd, dx, stream):
     if rstd.dtype != torch.float32 or rstd.numel() != rows:
         raise ValueError("rstd must be float32 with one value per row")
     dx = _like(dz, dx, "dx")
-    _check(op, getattr(lib(), op)(dt, rows, cols, _ptr(dz), _ptr(z), _ptr(rstd), _ptr(dx),
-                                  _stream(dz, stream)))
+    with torch.cuda.device(dz.device):   # launches go to the tensors' GPU
+        _check(op, getattr(lib(), op)(dt, rows, cols, _ptr(dz), _ptr(z), _ptr(rstd), _ptr(dx),
+                                      _stream(dz, stream)))
     return dx
 
 
@@ -338,7 +354,8 @@ def copy_bytes(src, dst, stream=None):
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() != nbytes:
         raise ValueError("src and dst must have the same byte size")
-    _check("lmbp_copy", lib().lmbp_copy(_ptr(src), _ptr(dst), nbytes, _stream(src, stream)))
+    with torch.cuda.device(src.device):   # launches go to the tensors' GPU
+        _check("lmbp_copy", lib().lmbp_copy(_ptr(src), _ptr(dst), nbytes, _stream(src, stream)))
     return dst
 
 
@@ -350,7 +367,7 @@ def linear_act_fwd(x, w, bias=None, act="gelu", y=None, codes=None, z=None, stor
     if act not in ("gelu", "silu"):
         raise ValueError("act must be 'gelu' or 'silu'")
     _dev(x, "x")
-    _dev(w, "w")
+    _on(w, x, "w")
     if x.dtype != torch.bfloat16 or w.dtype != torch.bfloat16:
         raise TypeError("linear_act_fwd takes bfloat16 x and w")
     if w.dim() != 2 or x.shape[-1] != w.shape[1]:
@@ -359,28 +376,29 @@ def linear_act_fwd(x, w, bias=None, act="gelu", y=None, codes=None, z=None, stor
     m = math.prod(x.shape[:-1])
     out_shape = (*x.shape[:-1], n)
     if bias is not None:
-        _dev(bias, "bias")
+        _on(bias, x, "bias")
         if bias.dtype != torch.bfloat16 or bias.numel() != n:
             raise ValueError("bias must be a bfloat16 tensor of n elements")
     if y is None:
         y = torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
     else:
-        _dev(y, "y")
+        _on(y, x, "y")
         if y.dtype != torch.bfloat16 or y.numel() != m * n:
             raise ValueError("y must be a bfloat16 tensor of m * n elements")
     if z is None and store_z:
         z = torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
     elif z is not None:
-        _dev(z, "z")
+        _on(z, x, "z")
         if z.dtype != torch.bfloat16 or z.numel() != m * n:
             raise ValueError("z must be a bfloat16 tensor of m * n elements")
     codes = _codes_out(m * n, x.device, codes)
     L = lib()
-    _check("linear_act_fwd", L.linear_act_fwd(ACT_GELU if act == "gelu" else ACT_SILU, BF16, m, n, k,
-                                              _ptr(x), _ptr(w),
-                                              _ptr(bias) if bias is not None else None,
-                                              _ptr(y), _ptr(codes),
-                                              _ptr(z) if z is not None else None, _stream(x, stream)))
+    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+        _check("linear_act_fwd", L.linear_act_fwd(ACT_GELU if act == "gelu" else ACT_SILU, BF16, m, n, k,
+                                                  _ptr(x), _ptr(w),
+                                                  _ptr(bias) if bias is not None else None,
+                                                  _ptr(y), _ptr(codes),
+                                                  _ptr(z) if z is not None else None, _stream(x, stream)))
     return (y, codes, z) if z is not None else (y, codes)
 
 
@@ -390,7 +408,7 @@ def linear_swiglu_fwd(x, w_gate, w_up, h=None, s=None, u=None, codes=None, g=Non
     h = SiLU(g) * u, s = SiLU(g), codes of g. Returns (h, s, u, codes) or, with store_g
     (or a g tensor given), (h, s, u, codes, g)."""
     for t, nm in ((x, "x"), (w_gate, "w_gate"), (w_up, "w_up")):
-        _dev(t, nm)
+        _on(t, x, nm)
         if t.dtype != torch.bfloat16:
             raise TypeError("linear_swiglu_fwd takes bfloat16 tensors")
     if w_gate.dim() != 2 or w_gate.shape != w_up.shape or x.shape[-1] != w_gate.shape[1]:
@@ -402,7 +420,7 @@ def linear_swiglu_fwd(x, w_gate, w_up, h=None, s=None, u=None, codes=None, g=Non
     def out(t, name):
         if t is None:
             return torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
-        _dev(t, name)
+        _on(t, x, name)
         if t.dtype != torch.bfloat16 or t.numel() != m * n:
             raise ValueError(f"{name} must be a bfloat16 tensor of m * n elements")
         return t
@@ -411,7 +429,8 @@ def linear_swiglu_fwd(x, w_gate, w_up, h=None, s=None, u=None, codes=None, g=Non
     if g is not None or store_g:
         g = out(g, "g")
     codes = _codes_out(m * n, x.device, codes)
-    _check("linear_swiglu_fwd", lib().linear_swiglu_fwd(
-        BF16, m, n, k, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(h), _ptr(s), _ptr(u), _ptr(codes),
-        _ptr(g) if g is not None else None, _stream(x, stream)))
+    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+        _check("linear_swiglu_fwd", lib().linear_swiglu_fwd(
+            BF16, m, n, k, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(h), _ptr(s), _ptr(u), _ptr(codes),
+            _ptr(g) if g is not None else None, _stream(x, stream)))
     return (h, s, u, codes, g) if g is not None else (h, s, u, codes)
