@@ -93,19 +93,27 @@ def load_traffic(kernel):
     return rec.get("traffic_bytes")
 
 
-def cpu_baseline(w, min_seconds=10.0):
-    """The CPU oracle, as it stands, on the whole step (every row of every tensor),
-    repeated until at least `min_seconds` of wall time; scaled to the same
-    algorithmic-bytes unit as the GPU value. NumPy runs these elementwise and
-    row-reduction ufuncs on one thread."""
+def _host_cpu():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def _oracle_step(spec, x, dz, g, dy, min_seconds):
+    """Run the oracle's step on the given rows until `min_seconds` have passed; returns
+    (passes, elapsed seconds). `spec` = (norm op, activation op, norm dtype, activation
+    dtype, eps): plain values, so that worker processes need not import the package."""
     import oracle
-    eps = float(np.float32(w.norm.eps))
-    x, dz, g, dy = w.norm_x(), w.norm_dz(), w.act_x(), w.act_dy()
-    dt_n, dt_a = w.norm.dtype, w.act.dtype
-    ofwd = {"msrms": oracle.msrms_fwd, "msln": oracle.msln_fwd}[w.norm.op]
-    obwd = {"msrms": oracle.msrms_bwd, "msln": oracle.msln_bwd}[w.norm.op]
-    afwd = {"resilu2": oracle.resilu2_fwd, "regelu2": oracle.regelu2_fwd}[w.act.op]
-    abwd = {"resilu2": oracle.resilu2_bwd, "regelu2": oracle.regelu2_bwd}[w.act.op]
+    norm_op, act_op, dt_n, dt_a, eps = spec
+    ofwd = {"msrms": oracle.msrms_fwd, "msln": oracle.msln_fwd}[norm_op]
+    obwd = {"msrms": oracle.msrms_bwd, "msln": oracle.msln_bwd}[norm_op]
+    afwd = {"resilu2": oracle.resilu2_fwd, "regelu2": oracle.regelu2_fwd}[act_op]
+    abwd = {"resilu2": oracle.resilu2_bwd, "regelu2": oracle.regelu2_bwd}[act_op]
     passes = 0
     t0 = time.perf_counter()
     while True:
@@ -118,26 +126,64 @@ def cpu_baseline(w, min_seconds=10.0):
         passes += 1
         elapsed = time.perf_counter() - t0
         if elapsed >= min_seconds:
-            break
+            return passes, elapsed
+
+
+def _oracle_chunk(job):
+    """Worker of the all-cores baseline: the oracle step on one row chunk."""
+    spec, x, dz, g, dy, min_seconds = job
+    return _oracle_step(spec, x, dz, g, dy, min_seconds)
+
+
+def _spec(w):
+    return (w.norm.op, w.act.op, w.norm.dtype, w.act.dtype, float(np.float32(w.norm.eps)))
+
+
+def cpu_baseline(w, tensors, min_seconds=10.0):
+    """The CPU oracle, as it stands, on the whole step (every row of every tensor),
+    repeated until at least `min_seconds` of wall time; scaled to the same
+    algorithmic-bytes unit as the GPU value. NumPy runs these elementwise and
+    row-reduction ufuncs on one thread."""
+    passes, elapsed = _oracle_step(_spec(w), *tensors, min_seconds)
     step_bytes = sum(algorithmic_bytes(w).values())
-    model = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            for line in f:
-                if line.startswith("model name"):
-                    model = line.split(":", 1)[1].strip()
-                    break
-    except OSError:
-        pass
     return {
         "value": round(passes * step_bytes / elapsed / 1e9, 4),
         "unit": "GB/s",
         "cores": 1,
-        "host_cpu": model,
+        "host_cpu": _host_cpu(),
         "host_cpus_visible": os.cpu_count(),
         "kind": "oracle",
         "sample": (f"{passes} full pass(es) of the step (all {w.norm.rows} rows of every tensor), "
                    f"fp64 NumPy, {elapsed:.2f} s wall"),
+    }
+
+
+def cpu_baseline_all_cores(w, tensors, procs, min_seconds=5.0):
+    """The same oracle on every host core at once: the step's rows split into `procs`
+    chunks, one worker process each (started fresh, before this process touches the
+    GPU), each repeating its chunk for `min_seconds`; rate = bytes of all chunk passes
+    over the longest worker's wall time."""
+    import multiprocessing as mp
+    step_bytes = sum(algorithmic_bytes(w).values())
+    x, dz, g, dy = tensors
+    rn, ra = w.norm.rows, w.act.rows
+    jobs = []
+    for i in range(procs):
+        a, b = rn * i // procs, rn * (i + 1) // procs
+        c, d = ra * i // procs, ra * (i + 1) // procs
+        jobs.append((_spec(w), x[a:b], dz[a:b], g[c:d], dy[c:d], min_seconds))
+    with mp.get_context("spawn").Pool(procs) as pool:
+        res = pool.map(_oracle_chunk, jobs)
+    # The chunks split the rows evenly (within one row), each 1/procs of the step.
+    passes = sum(p for p, _ in res) / procs
+    wall = max(e for _, e in res)
+    return {
+        "value": round(passes * step_bytes / wall / 1e9, 4),
+        "unit": "GB/s",
+        "cores": procs,
+        "kind": "oracle",
+        "sample": (f"{procs} worker processes, each {min_seconds:.0f}+ s of passes over 1/{procs} of the "
+                   f"step's rows; {passes:.2f} step-equivalents in {wall:.2f} s"),
     }
 
 
@@ -367,9 +413,23 @@ def main():
     if args.steps < 1 or args.warmup < 0:
         sys.exit("--steps must be >= 1 and --warmup >= 0")
 
+    from paper_2406_16282_amd import inputs
+
+    # The CPU oracle runs first: its worker processes start from a process that has not
+    # touched the GPU yet.
+    cpu = {}
+    if not args.no_cpu_baseline and not args.swiglu:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        w0 = inputs.WORKLOADS[WORKLOAD]
+        tensors = (w0.norm_x(), w0.norm_dz(), w0.act_x(), w0.act_dy())
+        cpu["cpu_baseline"] = cpu_baseline(w0, tensors)
+        procs = max(1, min(16, os.cpu_count() or 1))
+        print(f"[bench] timing the CPU oracle on {procs} processes", file=sys.stderr, flush=True)
+        cpu["cpu_baseline_all_cores"] = cpu_baseline_all_cores(w0, tensors, procs)
+        del tensors
+
     import torch
     import paper_2406_16282_amd as lmbp
-    from paper_2406_16282_amd import inputs
 
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
@@ -547,9 +607,7 @@ def main():
     if args.linear:
         print("[bench] fused linear + activation", file=sys.stderr, flush=True)
         out["linear"] = linear_report(torch, lmbp, inputs, dev, reps=max(10, min(args.steps, 50)))
-    if not args.no_cpu_baseline and not args.swiglu:
-        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w)
+    out.update(cpu)
     print(json.dumps(out))
 
 
