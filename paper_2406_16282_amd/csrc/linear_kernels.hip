@@ -25,8 +25,9 @@
 // hit distinct LDS banks; one load instruction of a wave fills 1 KiB (16 rows), lane l
 // writing unit l % 4 of row l / 4 (the row's four lanes read its 64 contiguous bytes in
 // permuted order). Within the loop the fragments of the next K slice (16) are read into
-// their own registers before the MFMAs of the current one, across step boundaries too;
-// the loop body is branch-free (loads past the last step read zeros into spent
+// their own registers while the MFMAs of the current one run (scheduling groups put one
+// MFMA between consecutive loads and reads), across step boundaries too; the loop body
+// is branch-free (loads past the last step read zeros into spent
 // buffers) so that the compiler's LDS waits are exact. Lane layout of the MFMA (checked
 // on the hardware): lane l supplies row l % 32 of A and column l % 32 of B at
 // k = 8 (l / 32) .. + 7, and holds result rows 8 (r / 4) + 4 (l / 32) + r % 4 of column
@@ -102,6 +103,24 @@ __device__ inline __amdgpu_buffer_rsrc_t make_rsrc(const uint16_t* base, int64_t
 // 16 bytes per lane from the buffer into LDS at `dst` + lane * 16 (dst wave-uniform).
 __device__ inline void load_lds16(__amdgpu_buffer_rsrc_t r, uint16_t* dst, uint32_t offset) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (lds_void*)dst, 16, offset, 0, 0, 0);
+}
+
+// Scheduling groups for one K slice: its MF MFMAs, with VM buffer loads and then DS LDS
+// reads spread over the first half of them (so the reads have landed before the slice
+// ends and the next wait finds nothing outstanding).
+template <int MF, int VM, int DS, int I = 0>
+__device__ inline void spread() {
+  if constexpr (I < MF) {
+    constexpr int W = MF / 2 < 1 ? 1 : MF / 2;
+    constexpr int T = VM + DS;
+    constexpr int lo = I < W ? T * I / W : T, hi = I < W ? T * (I + 1) / W : T;
+    constexpr int vm = (hi < VM ? hi : VM) - (lo < VM ? lo : VM);
+    constexpr int ds = (hi - lo) - vm;
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // one MFMA
+    if constexpr (vm > 0) __builtin_amdgcn_sched_group_barrier(0x020, vm, 0);  // buffer loads
+    if constexpr (ds > 0) __builtin_amdgcn_sched_group_barrier(0x100, ds, 0);  // LDS reads
+    spread<MF, VM, DS, I + 1>();
+  }
 }
 
 // Tile coordinates of this block (see the file comment).
@@ -240,6 +259,8 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
       for (int kk = 0; kk < kSlices; ++kk) {
         if (kk + 1 < kSlices) {
           read(S, kk + 1, (kk + 1) & 1);
+          mfmas(kk & 1);
+          spread<TM * TN, 0, TM + TN>();
         } else {
           // This wave's reads of step kt are complete once their data has arrived; after
           // the barrier every wave's are, and step kt + 1 is in LDS.
@@ -248,9 +269,10 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
           asm volatile("s_barrier" ::: "memory");
           issue_stage(kt + kStages);   // into step kt's buffer
           read(stage_ptr(kt + 1), 0, 0);
+          mfmas(kk & 1);
+          spread<TM * TN, C::kLoadsPerStage, TM + TN>();
         }
-        __builtin_amdgcn_sched_barrier(0);   // keep the reads ahead of the MFMAs
-        mfmas(kk & 1);
+        __builtin_amdgcn_sched_barrier(0);   // the slice's MFMAs stay ahead of the next wait
       }
     }
     const uint16_t* S = stage_ptr(kt_count - 1);
