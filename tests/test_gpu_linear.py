@@ -63,6 +63,8 @@ EXACT_SHAPES = [
     (200, 272, 200),     # several tiles, ragged m, n and K (K not a multiple of 64)
     (300, 384, 1024),    # many K steps
     (1, 16, 24),         # one row, one code-word column group
+    (256, 512, 96),      # K = three steps, two 128 x 128 tiles per column block
+    (130, 272, 104),     # ragged m and n, K three steps plus 8
 ]
 
 
@@ -73,17 +75,18 @@ def test_exact(m, n, k, act):
 
 
 @pytest.mark.parametrize("act", ["gelu", "silu"])
-def test_exact_large_tiles_ragged(act):
+@pytest.mark.parametrize("k", [520, 72])
+def test_exact_large_tiles_ragged(act, k):
     """A problem large enough for the 256 x 256 tile configuration (at least four rounds of
-    tiles), ragged in every dimension (m % 256 = 64, n % 256 = 16, k % 32 = 8); exact
-    dyadic arithmetic, compared on sampled rows that include the ragged last tile row."""
-    m, n, k = 8000, 8208, 520
+    tiles), ragged in every dimension (m % 256 = 64, n % 256 = 16, k % 32 = 8 for both K);
+    exact dyadic arithmetic, compared on sampled rows that include the ragged last tile row."""
+    m, n = 8000, 8208
     print(f"[linear] exact large tiles: m={m} n={n} k={k} act={act}", flush=True)
     x = inputs.dyadic((m, k), -3, tensor_id=inputs.LIN_X, block=1)
     w = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_W, block=1)
     b = inputs.dyadic((n,), -7, tensor_id=inputs.LIN_B, block=1)
     y, codes, z = run(x, w, b, act)
-    rows = np.unique(np.concatenate([[0, 255, 256, 7935, 7936, 7999],
+    rows = np.unique(np.concatenate([[0, 127, 128, 255, 256, 7935, 7936, 7999],
                                      np.random.default_rng(3).integers(0, m, 24)]))
     _, z_s, y_o, c_o = oracle.linear_act_fwd(x[rows], w, b, act)
     assert np.array_equal(z.reshape(m, n)[rows], z_s), "stored z differs from the exact rounding"
@@ -187,6 +190,7 @@ GLU_SHAPES = [
     (128, 64, 64),        # one small tile (64 output columns), one K step
     (200, 208, 200),      # several tiles, ragged m, n (n % 64 = 16) and K
     (8000, 4112, 520),    # large tiles (>= four rounds), ragged in every dimension
+    (8000, 4112, 88),     # the same with a short K (three steps)
 ]
 
 
@@ -200,7 +204,7 @@ def test_swiglu_exact(m, n, k):
     wu = inputs.dyadic((n, k), -4, tensor_id=inputs.LIN_B, block=m + n)
     h, s, u, codes, g = run_glu(x, wg, wu)
     rows = np.arange(m) if m <= 512 else np.unique(
-        np.concatenate([[0, 255, 256, m - 1], np.random.default_rng(5).integers(0, m, 20)]))
+        np.concatenate([[0, 127, 128, 255, 256, m - 1], np.random.default_rng(5).integers(0, m, 20)]))
     _, g_s, _, u_s, h_o, s_o, c_o = oracle.linear_swiglu_fwd(x[rows], wg, wu)
     assert np.array_equal(g.reshape(m, n)[rows], g_s), "g differs from the exact rounding"
     assert np.array_equal(u.reshape(m, n)[rows], u_s), "u differs from the exact rounding"
