@@ -133,9 +133,13 @@ def _on(t, ref, what):
 
 
 def _stream(t, stream):
+    """The HIP stream to launch on: the tensors' current stream by default, else a
+    torch.cuda.Stream of the same device or a raw stream handle."""
     if stream is None:
         return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
     if isinstance(stream, torch.cuda.Stream):
+        if stream.device != t.device:
+            raise ValueError(f"stream is on {stream.device}, the tensors on {t.device}")
         return ctypes.c_void_p(stream.cuda_stream)
     return ctypes.c_void_p(int(stream))
 
@@ -255,7 +259,11 @@ def stepact_fwd(x, act, thresholds, bits, y=None, codes=None, stream=None):
     ``thresholds`` are the 2^k - 1 increasing biases of the ReLU combination."""
     _dev(x, "x")
     dt = _dtype_code(x)
-    a = {"gelu": ACT_GELU, "silu": ACT_SILU}[act]
+    if act not in ("gelu", "silu"):
+        raise ValueError("act must be 'gelu' or 'silu'")
+    if bits not in (1, 2, 4):
+        raise ValueError("bits must be 1, 2 or 4")
+    a = ACT_GELU if act == "gelu" else ACT_SILU
     tab = _doubles(thresholds, (1 << bits) - 1, "thresholds")
     y = _like(x, y, "y")
     words = int(lib().lmbp_stepact_codes_bytes(bits, x.numel())) // 4
@@ -274,6 +282,8 @@ def stepact_bwd(dy, codes, levels, bits, dx=None, stream=None):
     _dev(dy, "dy")
     dt = _dtype_code(dy)
     _on(codes, dy, "codes")
+    if bits not in (1, 2, 4):
+        raise ValueError("bits must be 1, 2 or 4")
     words = int(lib().lmbp_stepact_codes_bytes(bits, dy.numel())) // 4
     if codes.dtype != torch.int32 or codes.numel() < words:
         raise ValueError("codes must be the int32 buffer written by the forward")
@@ -350,7 +360,7 @@ def msrms_bwd(dz, z, rstd, dx=None, stream=None):
 def copy_bytes(src, dst, stream=None):
     """Measurement utility: 16-byte vector copy of src into dst (same byte size)."""
     _dev(src, "src")
-    _dev(dst, "dst")
+    _on(dst, src, "dst")
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() != nbytes:
         raise ValueError("src and dst must have the same byte size")
