@@ -6,8 +6,9 @@ general k; Appendix I). Test infrastructure only (see the package docstring).
   a code of k bits per element selects the slope; slope on segment j is the sum of the
   first j weights.
 * ReGELU2-d (Appendix I): k = 2 constants fitted to GELU's derivative instead of GELU.
-* Packing: k bits per element, 32/k codes per 32-bit word, least significant first
-  (k in {1, 2, 4}).
+* Packing: k bits per element, floor(32/k) codes per 32-bit word, least significant
+  first (k in {1, 2, 3, 4}; for k = 3 that is 10 codes and the word's top two bits are
+  zero, so no code straddles two words).
 """
 
 import numpy as np
@@ -50,9 +51,9 @@ def words_for(bits, n):
 
 
 def pack_bits(codes, bits):
-    """k-bit codes, 32/k per uint32 word, least significant first, zero tail."""
-    if bits not in (1, 2, 4):
-        raise ValueError("bits must be 1, 2 or 4")
+    """k-bit codes, floor(32/k) per uint32 word, least significant first, zero tail."""
+    if bits not in (1, 2, 3, 4):
+        raise ValueError("bits must be 1, 2, 3 or 4")
     codes = np.asarray(codes).reshape(-1)
     per = 32 // bits
     words = np.zeros(words_for(bits, codes.size), dtype=np.uint32)

@@ -23,7 +23,7 @@ def test_k2_family_equals_the_k2_oracle():
         assert np.array_equal(V.pack_bits(V.family_code(x, c), 2), oracle.pack_codes(oracle.segment_code(x, c)))
 
 
-@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
 def test_levels_are_slopes_for_every_k(bits):
     r = np.random.default_rng(bits)
     m = (1 << bits) - 1
@@ -33,7 +33,7 @@ def test_levels_are_slopes_for_every_k(bits):
                               V.family_code, a, c) < 1e-8
 
 
-@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
 def test_pack_round_trip_and_layout(bits):
     per = 32 // bits
     r = np.random.default_rng(7)
@@ -56,3 +56,24 @@ def test_regelu2d_levels_match_gelu_derivative_roughly():
     c = V.REGELU2D_C
     assert d(-6) - 1e-3 < lv[0] < d(c[0]) + 1e-3
     assert d(c[0]) < lv[1] < d(c[1]) and d(c[1]) < lv[2] < d(c[2]) and d(c[2]) < lv[3] < 1.13
+
+
+def test_three_bit_layout_by_hand():
+    """k = 3: ten codes per word at bits 3j .. 3j + 2, top two bits zero, next word for
+    the eleventh code (written out bit by bit, independent of pack_bits)."""
+    codes = np.array([1, 2, 3, 4, 5, 6, 7, 0, 7, 6, 5], dtype=np.uint8)
+    w0 = sum(int(c) << (3 * j) for j, c in enumerate(codes[:10]))
+    assert list(V.pack_bits(codes, 3)) == [w0, 5]
+    assert int(V.pack_bits(np.full(10, 7, dtype=np.uint8), 3)[0]) == 0x3FFFFFFF
+    assert V.words_for(3, 10) == 1 and V.words_for(3, 11) == 2
+
+
+def test_three_bit_family_codes_brute_force():
+    """k = 3 (7 biases, 8 slopes): codes count the biases below x, per element."""
+    r = np.random.default_rng(33)
+    c = np.sort(r.uniform(-4, 4, 7))
+    x = r.normal(0, 3, 2000)
+    want = np.array([sum(1 for ci in c if xi > ci) for xi in x], dtype=np.uint8)
+    assert np.array_equal(V.family_code(x, c), want)
+    words = V.pack_bits(want, 3)
+    assert np.array_equal(V.unpack_bits(words, 3, x.size), want)
