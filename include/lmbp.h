@@ -128,8 +128,10 @@ lmbp_status reswiglu2_bwd(lmbp_dtype dt, int64_t n, const void *dh, const void *
  * the combination). Backward: dx = dy * levels[code] (2^k levels: the slopes of the
  * combination on its segments, cumulative sums of its weights).
  *
- *   bits       : k in {1, 2, 4}; codes hold 32/k elements per 32-bit word, least
- *                significant first, zero tail; lmbp_stepact_codes_bytes(k, n) bytes.
+ *   bits       : k in {1, 2, 3, 4}; codes hold floor(32/k) elements per 32-bit word
+ *                (32, 16, 10, 8), least significant first (code j of a word at bits
+ *                k j .. k j + k - 1; for k = 3 the top two bits are 0), zero tail;
+ *                lmbp_stepact_codes_bytes(k, n) bytes.
  *   thresholds : host array of 2^k - 1 finite, strictly increasing doubles (read
  *                during the call only). Each is applied as an exact real comparison.
  *   levels     : host array of 2^k finite doubles, used as fp32 values.

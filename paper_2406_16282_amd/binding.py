@@ -261,8 +261,8 @@ def stepact_fwd(x, act, thresholds, bits, y=None, codes=None, stream=None):
     dt = _dtype_code(x)
     if act not in ("gelu", "silu"):
         raise ValueError("act must be 'gelu' or 'silu'")
-    if bits not in (1, 2, 4):
-        raise ValueError("bits must be 1, 2 or 4")
+    if bits not in (1, 2, 3, 4):
+        raise ValueError("bits must be 1, 2, 3 or 4")
     a = ACT_GELU if act == "gelu" else ACT_SILU
     tab = _doubles(thresholds, (1 << bits) - 1, "thresholds")
     y = _like(x, y, "y")
@@ -282,8 +282,8 @@ def stepact_bwd(dy, codes, levels, bits, dx=None, stream=None):
     _dev(dy, "dy")
     dt = _dtype_code(dy)
     _on(codes, dy, "codes")
-    if bits not in (1, 2, 4):
-        raise ValueError("bits must be 1, 2 or 4")
+    if bits not in (1, 2, 3, 4):
+        raise ValueError("bits must be 1, 2, 3 or 4")
     words = int(lib().lmbp_stepact_codes_bytes(bits, dy.numel())) // 4
     if codes.dtype != torch.int32 or codes.numel() < words:
         raise ValueError("codes must be the int32 buffer written by the forward")

@@ -132,7 +132,7 @@ uint64_t step_codes_bytes(int bits, int64_t n) {
   return n <= 0 ? 0 : (uint64_t(n) + per - 1) / per * 4;
 }
 
-bool valid_bits(int bits) { return bits == 1 || bits == 2 || bits == 4; }
+bool valid_bits(int bits) { return bits >= 1 && bits <= 4; }
 
 // Largest fp32 value not above c (for finite c within the fp32 range).
 float round_down_f32(double c) {

@@ -141,7 +141,7 @@ def fit(act, bits=2, kind="function", starts=8, seed=0, anneal=False, x0=None):
 def main():
     ap = argparse.ArgumentParser(description="Fit a ReLU combination to GELU or SiLU")
     ap.add_argument("--act", choices=("gelu", "silu"), default="gelu")
-    ap.add_argument("--bits", type=int, choices=(1, 2, 4), default=2)
+    ap.add_argument("--bits", type=int, choices=(1, 2, 3, 4), default=2)
     ap.add_argument("--objective", choices=("function", "derivative"), default="function")
     ap.add_argument("--starts", type=int, default=8)
     ap.add_argument("--anneal", action="store_true", help="seed the search with dual annealing")

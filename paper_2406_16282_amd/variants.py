@@ -28,10 +28,10 @@ def levels_of(a):
 
 def bits_of(c):
     m = len(c)
-    for k in (1, 2, 4):
+    for k in (1, 2, 3, 4):
         if m == (1 << k) - 1:
             return k
-    raise ValueError("the number of biases must be 1, 3 or 15 (k = 1, 2, 4)")
+    raise ValueError("the number of biases must be 1, 3, 7 or 15 (k = 1, 2, 3, 4)")
 
 
 class _Step(torch.autograd.Function):

@@ -195,7 +195,11 @@ def test_stepact_errors(L):
     f, b = L.stepact_fwd, L.stepact_bwd
     x, y, c = P, P + 4096, P + 8192
     assert f(0, 2, t3, 7, 16, x, y, c, None) == B.EDTYPE
-    assert f(0, 3, t3, B.BF16, 16, x, y, c, None) == B.EINVAL     # k = 3 not supported
+    assert f(0, 5, t3, B.BF16, 16, x, y, c, None) == B.EINVAL     # k = 5 not supported
+    assert f(0, 0, t3, B.BF16, 16, x, y, c, None) == B.EINVAL     # nor k = 0
+    t7 = (ctypes.c_double * 7)(-3.0, -2.0, -1.0, 0.0, 1.0, 2.0, 3.0)
+    assert f(0, 3, t7, B.BF16, 0, x, y, c, None) == B.OK          # k = 3: seven thresholds
+    assert b(3, (ctypes.c_double * 8)(*range(8)), B.BF16, 0, x, c, y, None) == B.OK
     assert f(5, 2, t3, B.BF16, 16, x, y, c, None) == B.EINVAL     # unknown activation
     assert f(0, 2, None, B.BF16, 16, x, y, c, None) == B.EINVAL
     assert f(0, 2, bad, B.BF16, 16, x, y, c, None) == B.EINVAL
@@ -204,4 +208,5 @@ def test_stepact_errors(L):
     assert f(0, 2, t3, B.BF16, 16, x, x + 2, c, None) == B.EOVERLAP
     assert b(2, None, B.BF16, 16, x, c, y, None) == B.EINVAL
     assert b(2, lv4, B.BF16, 16, x, x + 4, y, None) == B.EOVERLAP
-    assert [L.lmbp_stepact_codes_bytes(k, 33) for k in (1, 2, 3, 4)] == [8, 12, 0, 20]
+    # words of floor(32/k) codes: 2, 3, 4 (10 per word), 5 words for 33 elements; k = 5: 0
+    assert [L.lmbp_stepact_codes_bytes(k, 33) for k in (1, 2, 3, 4, 5)] == [8, 12, 16, 20, 0]

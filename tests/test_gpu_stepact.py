@@ -47,7 +47,7 @@ def check(act, bits, a, c, dtype, x, dy, label):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
-@pytest.mark.parametrize("bits", [1, 2, 4])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
 @pytest.mark.parametrize("act", ["gelu", "silu"])
 def test_random_tables(act, bits, dtype):
     a, c = tables(bits, seed=bits)
@@ -101,3 +101,39 @@ def test_fitted_four_bit_gelu(dtype):
     x = inputs.edge_activation(shape, dtype, list(c))
     dy = inputs.normal(shape, 1.0, dtype, tensor_id=inputs.ACT_DY)
     check("gelu", 4, list(a), list(c), dtype, x, dy, "fitted k=4")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_fitted_three_bit_silu(dtype):
+    """A k = 3 member (7 biases, 8 slopes; ten codes per word) fitted by the offline search,
+    on inputs crowded at its thresholds, with a ragged tail (n % 640 != 0, n % 10 = 6)."""
+    from paper_2406_16282_amd import fit
+    a, c, _ = fit.fit("silu", 3, starts=1)
+    shape = (97, 2998)
+    x = inputs.edge_activation(shape, dtype, list(c))
+    dy = inputs.normal(shape, 1.0, dtype, tensor_id=inputs.ACT_DY)
+    check("silu", 3, list(a), list(c), dtype, x, dy, "fitted k=3")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+def test_three_bit_unaligned_and_in_place(dtype):
+    """k = 3 through the general path (base pointer one element off 16-byte alignment) and
+    in place (y == x, dx == dy), against the oracle."""
+    a, c = tables(3, seed=9)
+    n = 6403
+    x = inputs.normal((n + 1,), 3.0, dtype, tensor_id=inputs.ACT_X)
+    dy = inputs.normal((n + 1,), 1.0, dtype, tensor_id=inputs.ACT_DY)
+    lv = OV.family_levels(a)
+    y_o, w_o = OV.stepact_fwd(oracle.decode(x[1:], dtype), "gelu", c, 3)
+    dx_o = OV.stepact_bwd(oracle.decode(dy[1:], dtype), w_o, lv, 3)
+    tx, tdy = T(x), T(dy)
+    y, codes = lmbp.stepact_fwd(tx[1:], "gelu", c, 3)
+    dx = lmbp.stepact_bwd(tdy[1:], T(w_o), variants.levels_of(a), 3)
+    xi = T(x[1:].copy())
+    lmbp.stepact_fwd(xi, "gelu", c, 3, y=xi)
+    torch.cuda.synchronize()
+    assert_codes_equal(H(codes), w_o, "unaligned k=3 codes")
+    assert np.array_equal(H(y), H(xi)), "in-place y differs"
+    rtol = rtol_for(dtype)
+    assert_rel(oracle.decode(H(y), dtype), y_o, rtol, "unaligned k=3 y")
+    assert_rel(oracle.decode(H(dx), dtype), dx_o, rtol, "unaligned k=3 dx", floor=0.0)
