@@ -55,16 +55,16 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
 constexpr int kBK = 32;       // K step: one LDS stage row is 64 bytes
-constexpr int kStages = 4;    // LDS ring
 constexpr int kSlices = kBK / 16;
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 constexpr uint32_t kBufferGDword3 = 0x00020000;  // raw 32-bit buffer, gfx9 family
 constexpr uint32_t kOutOfRange = 0x80000000u;    // beyond any resource's range: reads 0
 
-template <int BM_, int BN_, int WM_, int WN_>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_ = 4>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
+  static constexpr int kStages = STAGES_;   // LDS ring
   static constexpr int kWaves = WM * WN;
   static constexpr int kThreads = kWaves * kWave;
   static constexpr int TM = BM / WM / 32, TN = BN / WN / 32;   // MFMA tiles per wave
@@ -81,7 +81,7 @@ struct Tile {
   static_assert((BM / 16) % kWaves == 0 && (BN / 16) % kWaves == 0, "load blocks per wave");
   static_assert(kThreads % kEpiThreadsPerRow == 0, "epilogue mapping");
   static_assert(kLdsElems * 2 <= 160 * 1024, "LDS per block");
-  static_assert((kStages - 1) * kLoadsPerStage <= 63, "vector-memory counter range");
+  static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerStage <= 63, "vector-memory counter range");
 };
 
 #ifndef LMBP_LIN_SMALL
@@ -203,6 +203,7 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
     const int row = (wave + kWaves * q) * 16 + r_in - ((GLU && q >= C::kLB / 2) ? BN / 2 : 0);
     ld_b[q] = uint32_t(row * K * 2 + kc * 16);
   }
+  constexpr int kStages = C::kStages;
   auto stage_ptr = [&](int64_t kt) { return lds + int(kt % kStages) * C::kStageElems; };
   auto issue_stage = [&](int64_t kt) {
     uint16_t* S = stage_ptr(kt);
