@@ -173,3 +173,87 @@ def test_fused_linear_swiglu_module():
     assert_mixed(oracle.decode(H(xt.grad), "bf16"), dg_o @ wgd + du_o @ wud, 2e-2, "swiglu module dx")
     assert_mixed(oracle.decode(H(mod.gate.weight.grad), "bf16"), dg_o.T @ xd, 2e-2, "swiglu module dWg")
     assert_mixed(oracle.decode(H(mod.up.weight.grad), "bf16"), du_o.T @ xd, 2e-2, "swiglu module dWu")
+
+
+def _saved_activation_bytes(run, params):
+    """Bytes of the distinct tensors autograd saves during `run()`, parameters excluded
+    (tensors sharing storage are counted once, as autograd keeps them once)."""
+    saved = []
+    with torch.autograd.graph.saved_tensors_hooks(lambda t: (saved.append(t), t)[1], lambda t: t):
+        out = run()
+    skip = {p.data_ptr() for p in params}
+    storages = {}
+    for t in saved:
+        st = t.untyped_storage()
+        if t.data_ptr() in skip:
+            continue
+        storages[st.data_ptr()] = st.nbytes()
+    return sum(storages.values()), out
+
+
+def test_vit_mlp_block_activation_memory():
+    """A ViT-B MLP block (norm, 768 -> 3072, GELU, 3072 -> 768; bf16, 256 tokens): the
+    standard torch block against MS-LN + ReGELU2 (Sec. 4-5), unfused and with the fused
+    linear + activation. Ours keeps, per token, z (2p B, shared by the norm and fc1), rstd
+    (4 B), the 2-bit codes (F/4 B) and fc2's input (2F B), exactly."""
+    from paper_2406_16282_amd.nn import LinearReGELU2
+    tok, p, f = 256, 768, 3072
+    x = torch.randn(tok, p, device=DEV, dtype=torch.bfloat16)
+    ln = nn.LayerNorm(p, eps=1e-6, device=DEV, dtype=torch.bfloat16)
+    fc1 = nn.Linear(p, f, device=DEV, dtype=torch.bfloat16)
+    fc2 = nn.Linear(f, p, device=DEV, dtype=torch.bfloat16)
+    xs = x.clone().requires_grad_(True)
+    std, _ = _saved_activation_bytes(lambda: fc2(nn.functional.gelu(fc1(ln(xs)))),
+                                     list(ln.parameters()) + list(fc1.parameters()) + list(fc2.parameters()))
+    ms = MSLayerNorm(1e-6)
+    act = ReGELU2()
+    params = list(fc1.parameters()) + list(fc2.parameters())
+    xo = x.clone().requires_grad_(True)
+    ours, _ = _saved_activation_bytes(lambda: fc2(act(fc1(ms(xo)))), params)
+    fused = LinearReGELU2(p, f, device=DEV)
+    xf = x.clone().requires_grad_(True)
+    ours_fused, _ = _saved_activation_bytes(lambda: fc2(fused(ms(xf))),
+                                            params + list(fused.parameters()))
+    want = tok * (2 * p + 4 + f // 4 + 2 * f)
+    print(f"[nn] ViT-B MLP block saved bytes per token: torch {std / tok:.0f}, "
+          f"MS-LN + ReGELU2 {ours / tok:.0f}, fused {ours_fused / tok:.0f}", flush=True)
+    assert ours == want and ours_fused == want
+    assert std >= tok * (4 * p + 4 * f)       # x, norm output, fc1 output, GELU output
+    assert ours / std < 0.56
+
+
+def test_llama_mlp_block_activation_memory():
+    """A LLaMA-7B MLP block (RMSNorm, gate and up 4096 -> 11008, SwiGLU, down 11008 -> 4096;
+    bf16, 64 tokens): standard torch against MS-RMSNorm + ReSwiGLU2 (unfused) and the fused
+    gate/up + SwiGLU layer. Ours keeps z (2p, shared), rstd (4), codes of g (F/4), u and
+    s = SiLU(g) (2F each), and the down projection's input h (2F) per token."""
+    from paper_2406_16282_amd.nn import LinearReSwiGLU2
+    tok, p, f = 64, 4096, 11008
+    x = torch.randn(tok, p, device=DEV, dtype=torch.bfloat16)
+    rms = nn.RMSNorm(p, eps=1e-5, device=DEV, dtype=torch.bfloat16)
+    gate = nn.Linear(p, f, bias=False, device=DEV, dtype=torch.bfloat16)
+    up = nn.Linear(p, f, bias=False, device=DEV, dtype=torch.bfloat16)
+    down = nn.Linear(f, p, bias=False, device=DEV, dtype=torch.bfloat16)
+    params = [gate.weight, up.weight, down.weight]
+    xs = x.clone().requires_grad_(True)
+
+    def standard():
+        z = rms(xs)
+        return down(nn.functional.silu(gate(z)) * up(z))
+    std, _ = _saved_activation_bytes(standard, params + [rms.weight])
+    ms, glu = MSRMSNorm(1e-5), ReSwiGLU2()
+    xo = x.clone().requires_grad_(True)
+
+    def ours_fn():
+        z = ms(xo)
+        return down(glu(gate(z), up(z)))
+    ours, _ = _saved_activation_bytes(ours_fn, params)
+    fused = LinearReSwiGLU2(p, f, device=DEV)
+    xf = x.clone().requires_grad_(True)
+    ours_fused, _ = _saved_activation_bytes(lambda: down(fused(ms(xf))),
+                                            params + [fused.gate.weight, fused.up.weight])
+    print(f"[nn] LLaMA-7B MLP block saved bytes per token: torch {std / tok:.0f}, "
+          f"MS-RMSNorm + ReSwiGLU2 {ours / tok:.0f}, fused {ours_fused / tok:.0f}", flush=True)
+    assert ours_fused == tok * (2 * p + 4 + f // 4 + 3 * 2 * f)
+    assert ours == ours_fused
+    assert ours < std
