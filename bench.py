@@ -287,6 +287,28 @@ LINEAR_SHAPES = {
 LINEAR_GLU_SHAPE = (4 * 2048, 11008, 4096)   # LLaMA-7B MLP: x [m, k], gate and up [n, k]
 
 
+def _timed_all(torch, fns, reps, trials=5):
+    """Median over `trials` of the mean duration (us) of `reps` back-to-back calls, the
+    trials of the callables interleaved (so clock drift affects all alike), after a
+    warm-up of the same length (the clocks ramp up under load)."""
+    mk = lambda: torch.cuda.Event(enable_timing=True)
+    for fn in fns:
+        for _ in range(reps):
+            fn()
+    torch.cuda.synchronize()
+    res = [[] for _ in fns]
+    for _ in range(trials):
+        for i, fn in enumerate(fns):
+            a, b = mk(), mk()
+            a.record()
+            for _ in range(reps):
+                fn()
+            b.record()
+            torch.cuda.synchronize()
+            res[i].append(a.elapsed_time(b) * 1e3 / reps)
+    return [float(np.median(r)) for r in res]
+
+
 def linear_report(torch, lmbp, inputs, dev, reps):
     """Fused linear + ReGELU2 / ReSiLU2 forward against the unfused sequence (library
     GEMM through torch, i.e. hipBLASLt, writing z, then the activation kernel reading
@@ -294,26 +316,7 @@ def linear_report(torch, lmbp, inputs, dev, reps):
     back-to-back launches on the current stream, median of five trials interleaved
     across the four variants after a warm-up of the same length."""
     out = {}
-    mk = lambda: torch.cuda.Event(enable_timing=True)
-
-    def timed_all(fns, trials=5):
-        """Median over `trials` of the mean duration of `reps` back-to-back launches,
-        the trials of the callables interleaved (so clock drift affects all alike)."""
-        for fn in fns:             # warm-up: the clocks ramp up under load
-            for _ in range(reps):
-                fn()
-        torch.cuda.synchronize()
-        res = [[] for _ in fns]
-        for _ in range(trials):
-            for i, fn in enumerate(fns):
-                a, b = mk(), mk()
-                a.record()
-                for _ in range(reps):
-                    fn()
-                b.record()
-                torch.cuda.synchronize()
-                res[i].append(a.elapsed_time(b) * 1e3 / reps)
-        return [float(np.median(r)) for r in res]
+    timed_all = lambda fns: _timed_all(torch, fns, reps)
 
     for name, (m, n, k, act, has_bias) in LINEAR_SHAPES.items():
         T = lambda a: inputs.storage_to_torch(a, dev)
@@ -391,6 +394,75 @@ def linear_report(torch, lmbp, inputs, dev, reps):
     return out
 
 
+BLOCK_SHAPES = {
+    # name: (tokens, hidden p, MLP width F, architecture)
+    "vit_b_bs64_mlp_bf16": (64 * 197, 768, 3072, "vit"),
+    "llama7b_mlp_bf16": (4 * 2048, 4096, 11008, "llama"),
+}
+
+
+def block_report(torch, dev, reps):
+    """Training step (forward + backward with input and weight gradients) of a whole MLP
+    block in bf16, torch's modules against this library's: MS-LN / MS-RMSNorm (the norm's
+    affine merged into the next layer), the first projection fused with ReGELU2 (ViT-B) or
+    with ReSiLU2 inside SwiGLU (LLaMA-7B), then the library's plain second projection. Step
+    time: median of interleaved trials of `reps` steps; memory: the bytes the forward leaves
+    allocated for the backward (all saved activations, beyond the inputs and the output)."""
+    from torch import nn
+    from paper_2406_16282_amd.nn import LinearReGELU2, LinearReSwiGLU2, MSLayerNorm, MSRMSNorm
+    bf = dict(device=dev, dtype=torch.bfloat16)
+    out = {}
+    for name, (tok, p, f, arch) in BLOCK_SHAPES.items():
+        gen = torch.Generator(device=dev).manual_seed(0)
+        x = torch.randn(tok, p, generator=gen, **bf)
+        dy = torch.randn(tok, p, generator=gen, **bf) * 1e-2
+        if arch == "vit":
+            ln, fc1, fc2 = nn.LayerNorm(p, eps=1e-6, **bf), nn.Linear(p, f, **bf), nn.Linear(f, p, **bf)
+            ms, fused, fc2b = MSLayerNorm(1e-6), LinearReGELU2(p, f, device=dev), nn.Linear(f, p, **bf)
+            torch_block = lambda xi: fc2(nn.functional.gelu(fc1(ln(xi))))
+            our_block = lambda xi: fc2b(fused(ms(xi)))
+        else:
+            rms = nn.RMSNorm(p, eps=1e-5, **bf)
+            gate, up, down = (nn.Linear(p, f, bias=False, **bf), nn.Linear(p, f, bias=False, **bf),
+                              nn.Linear(f, p, bias=False, **bf))
+            ms, fused, downb = MSRMSNorm(1e-5), LinearReSwiGLU2(p, f, device=dev), nn.Linear(f, p, bias=False, **bf)
+
+            def torch_block(xi):
+                z = rms(xi)
+                return down(nn.functional.silu(gate(z)) * up(z))
+            our_block = lambda xi: downb(fused(ms(xi)))
+
+        def step(block):
+            xi = x.detach().requires_grad_(True)
+            block(xi).backward(dy)
+
+        def kept_bytes(block):
+            step(block)                      # gradients allocated before the measurement
+            torch.cuda.synchronize()
+            xi = x.detach().requires_grad_(True)
+            before = torch.cuda.memory_allocated()
+            y = block(xi)
+            torch.cuda.synchronize()
+            kept = torch.cuda.memory_allocated() - before - y.numel() * y.element_size()
+            del y, xi
+            return kept
+
+        mem_t, mem_o = kept_bytes(torch_block), kept_bytes(our_block)
+        t_torch, t_ours = _timed_all(torch, [lambda: step(torch_block), lambda: step(our_block)], reps)
+        out[name] = {
+            "tokens": tok, "hidden": p, "mlp": f,
+            "torch_step_us": round(t_torch, 1), "ours_step_us": round(t_ours, 1),
+            "speedup": round(t_torch / t_ours, 3),
+            "torch_kept_bytes_per_token": round(mem_t / tok, 1),
+            "ours_kept_bytes_per_token": round(mem_o / tok, 1),
+            "memory_ratio": round(mem_o / mem_t, 4),
+        }
+        print(f"[bench] block {name}: step {t_torch:.1f} us torch vs {t_ours:.1f} us ours; activations "
+              f"{mem_t / tok:.0f} vs {mem_o / tok:.0f} B/token", file=sys.stderr, flush=True)
+        torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -401,6 +473,9 @@ def main():
                     help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
     ap.add_argument("--pairs", action="store_true",
                     help="also report forward+backward GB/s of each op pair on every workload")
+    ap.add_argument("--blocks", action="store_true",
+                    help="also report the training step time and kept activation memory of whole "
+                         "ViT-B and LLaMA-7B MLP blocks, torch modules against this library's")
     ap.add_argument("--linear", action="store_true",
                     help="also report the fused linear + activation forward against the unfused "
                          "library GEMM + activation kernel")
@@ -609,6 +684,9 @@ def main():
     if args.linear:
         print("[bench] fused linear + activation", file=sys.stderr, flush=True)
         out["linear"] = linear_report(torch, lmbp, inputs, dev, reps=max(10, min(args.steps, 50)))
+    if args.blocks:
+        print("[bench] MLP blocks", file=sys.stderr, flush=True)
+        out["blocks"] = block_report(torch, dev, reps=max(5, min(args.steps, 20)))
     out.update(cpu)
     print(json.dumps(out))
 

@@ -99,9 +99,11 @@ class _LinearAct(torch.autograd.Function):
         x2, weight, codes = ctx.saved_tensors
         bwd = binding.regelu2_bwd if ctx.which == "gelu" else binding.resilu2_bwd
         dz = bwd(_flat(dy).reshape(-1, weight.shape[0]), codes)
+        # The two products of a linear layer's backward, as torch's own linear layer forms
+        # them (2-D GEMMs; the transposed left operand is read in place by the library).
         dx = (dz @ weight).reshape(ctx.x_shape) if ctx.needs_input_grad[0] else None
-        dw = (dz.t().contiguous() @ x2) if ctx.needs_input_grad[1] else None
-        db = dz.float().sum(0).to(dz.dtype) if ctx.has_bias and ctx.needs_input_grad[2] else None
+        dw = dz.t().mm(x2) if ctx.needs_input_grad[1] else None
+        db = dz.sum(0, dtype=torch.float32).to(dz.dtype) if ctx.has_bias and ctx.needs_input_grad[2] else None
         return dx, dw, db, None
 
 
@@ -140,9 +142,9 @@ class _LinearSwiGLU(torch.autograd.Function):
     def backward(ctx, dh):
         x2, w_gate, w_up, s, u, codes = ctx.saved_tensors
         dg, du = binding.reswiglu2_bwd(_flat(dh).reshape(-1, w_gate.shape[0]), u, s, codes)
-        dx = ((dg @ w_gate) + (du @ w_up)).reshape(ctx.x_shape) if ctx.needs_input_grad[0] else None
-        dwg = (dg.t().contiguous() @ x2) if ctx.needs_input_grad[1] else None
-        dwu = (du.t().contiguous() @ x2) if ctx.needs_input_grad[2] else None
+        dx = torch.addmm(dg @ w_gate, du, w_up).reshape(ctx.x_shape) if ctx.needs_input_grad[0] else None
+        dwg = dg.t().mm(x2) if ctx.needs_input_grad[1] else None
+        dwu = du.t().mm(x2) if ctx.needs_input_grad[2] else None
         return dx, dwg, dwu
 
 
