@@ -82,6 +82,23 @@ __device__ inline void stg16(void* base, int64_t vec_index, const u32x4& v) {
   else *p = v;
 }
 
+// Wave index within the block as a wave-uniform (scalar) value.
+__device__ inline int wave_in_block() {
+  return __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+}
+
+// Buffer resource over the 16-byte vectors [vbase, vbase + nvec) of `base` (both
+// wave-uniform), and a 16-byte store through it with cache policy CPOL (buffer
+// instruction bits: sc0 = 1, nt = 2, sc1 = 16).
+__device__ inline __amdgpu_buffer_rsrc_t vec_rsrc(void* base, int64_t vbase, int64_t nvec) {
+  return __builtin_amdgcn_make_buffer_rsrc(static_cast<char*>(base) + vbase * 16, 0, int(nvec * 16),
+                                           0x00020000);
+}
+template <int CPOL = 2 | 16>
+__device__ inline void stb16(__amdgpu_buffer_rsrc_t r, int idx, const u32x4& v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, idx * 16, 0, CPOL);
+}
+
 // Compiler-only barrier: makes `v` opaque so that values derived from it are
 // recomputed after this point instead of being kept live in registers.
 __device__ inline void opaque(u32x4& v) { asm volatile("" : "+v"(v)); }

@@ -21,11 +21,9 @@
 namespace lmbp {
 
 #ifndef LMBP_NORM_NT
-// Non-temporal loads (bit 0) / stores (bit 1). Inputs and outputs are touched
-// once per launch, so both stream past the caches; measured on the whole step,
-// this beats default-policy loads even though a norm kernel alone reads faster
-// with them (the next kernels pay for the cached lines).
-#define LMBP_NORM_NT 3
+// Non-temporal loads (bit 0). Inputs are touched once per launch, so they stream past
+// the caches (cold, default-policy loads were slower).
+#define LMBP_NORM_NT 1
 #endif
 #ifndef LMBP_NORM_FWD_NT
 #define LMBP_NORM_FWD_NT LMBP_NORM_NT  // the forward kernel's policy
@@ -33,10 +31,13 @@ namespace lmbp {
 #ifndef LMBP_NORM_BWD_NT
 #define LMBP_NORM_BWD_NT LMBP_NORM_NT  // the backward kernel's policy
 #endif
+#ifndef LMBP_NORM_STORE_CPOL
+// Cache policy of the 16-byte stores (buffer instructions): non-temporal (2). Stores at
+// device scope (sc1), with or without nt, were slower here when the outputs are cold.
+#define LMBP_NORM_STORE_CPOL 2
+#endif
 constexpr bool kFwdNtLoad = (LMBP_NORM_FWD_NT & 1) != 0;
-constexpr bool kFwdNtStore = (LMBP_NORM_FWD_NT & 2) != 0;
 constexpr bool kBwdNtLoad = (LMBP_NORM_BWD_NT & 1) != 0;
-constexpr bool kBwdNtStore = (LMBP_NORM_BWD_NT & 2) != 0;
 
 // Threads per block of the register-tile path: 256, or one row of WPR waves when
 // that is wider (WPR = 8).
@@ -80,7 +81,7 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_fwd_vec(const void* x,
   constexpr int RPB = norm_block<WPR>() / TPR;
   __shared__ float red[2][norm_block<WPR>() / kWave];
   const int t = threadIdx.x % TPR;
-  const int64_t row = int64_t(blockIdx.x) * RPB + threadIdx.x / TPR;
+  const int64_t row = int64_t(blockIdx.x) * RPB + wave_in_block() / WPR;
   const bool active = row < rows;
   if constexpr (WPR == 1) {
     if (!active) return;  // no barriers in the single-wave path
@@ -138,7 +139,7 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_fwd_vec(const void* x,
       IO::unpack(v[j], f);
 #pragma unroll
       for (int e = 0; e < E; ++e) f[e] = (LN ? (f[e] - pivot) - mean_d : f[e]) * rs;
-      stg16<kFwdNtStore>(z, vbase + idx, IO::pack(f));
+      stb16<LMBP_NORM_STORE_CPOL>(vec_rsrc(z, vbase, nv), idx, IO::pack(f));
     }
   }
   if (t == 0) rstd[row] = rs;
@@ -153,7 +154,7 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_bwd_vec(const void* dz
   constexpr int RPB = norm_block<WPR>() / TPR;
   __shared__ float red[2][norm_block<WPR>() / kWave];
   const int t = threadIdx.x % TPR;
-  const int64_t row = int64_t(blockIdx.x) * RPB + threadIdx.x / TPR;
+  const int64_t row = int64_t(blockIdx.x) * RPB + wave_in_block() / WPR;
   const bool active = row < rows;
   if constexpr (WPR == 1) {
     if (!active) return;
@@ -200,7 +201,7 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_bwd_vec(const void* dz
       IO::unpack(vz[j], zz);
 #pragma unroll
       for (int e = 0; e < E; ++e) g[e] = rs * __builtin_fmaf(-zz[e], b, g[e] - a);
-      stg16<kBwdNtStore>(dx, vbase + idx, IO::pack(g));
+      stb16<LMBP_NORM_STORE_CPOL>(vec_rsrc(dx, vbase, nv), idx, IO::pack(g));
     }
   }
 }
