@@ -675,6 +675,9 @@ def main():
         # Step time minus the per-kernel durations measured in their own loops: the gaps
         # between launches (a few us; within run-to-run noise it can come out slightly negative).
         "step_minus_kernel_sum_us": round(ms_step * 1e3 - sum(per_kernel_ms.values()) * 1e3, 2),
+        # The step's bytes over the sum of the four kernels' own launch durations (the pairs'
+        # (B_fwd + B_bwd) / (t_fwd + t_bwd) summed over both pairs); `value` is the wall-clock rate.
+        "kernels_only_GBps": round(bytes_step / (sum(per_kernel_ms.values()) * 1e-3) / 1e9, 1),
         "wall_s_timed": round(t_wall, 4),
     }
     if args.pairs:
