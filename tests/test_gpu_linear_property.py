@@ -2,6 +2,8 @@
 m, n (multiple of 16), k (multiple of 8), activation and bias on dyadic inputs, whose
 fp32 accumulation is exact in any order, so z, u and codes compare bit for bit."""
 
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -14,7 +16,10 @@ from compare import assert_mixed, assert_rel
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
-SETTINGS = settings(max_examples=25, deadline=None, derandomize=True,
+# LMBP_PROPERTY_EXAMPLES raises the number of cases; LMBP_PROPERTY_RANDOM=1 draws them afresh
+# (the default is a fixed, derandomized set).
+SETTINGS = settings(max_examples=int(os.environ.get("LMBP_PROPERTY_EXAMPLES", 25)), deadline=None,
+                    derandomize=os.environ.get("LMBP_PROPERTY_RANDOM", "0") != "1", database=None,
                     suppress_health_check=[HealthCheck.too_slow])
 
 
