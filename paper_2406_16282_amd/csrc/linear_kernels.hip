@@ -15,16 +15,17 @@
 // of 128 x 64 for large problems, 128 x 128 with 4 waves of 64 x 64 (two blocks per CU)
 // when the large tiles would leave much of the last round of the GPU idle.
 //
-// K loop. K advances in steps of 32 through a ring of four LDS stages filled straight
-// from HBM by raw buffer loads with an LDS destination (buffer_load_dwordx4 ... lds):
-// up to four steps of loads are in flight and no register staging is needed. The
-// buffer resources end at the tile's last valid row, so ragged tiles read zeros
-// without branches, and chunks beyond K are pointed past the end to read zeros too.
-// A stage row is 32 bf16 = four 16-byte units, unit u of row r holding k-chunk
-// u ^ ((r >> 2) & 3), so that the operand reads of 16 consecutive rows at one k-chunk
-// hit distinct LDS banks; one load instruction of a wave fills 1 KiB (16 rows), lane l
-// writing unit l % 4 of row l / 4 (the row's four lanes read its 64 contiguous bytes in
-// permuted order). Within the loop the fragments of the next K slice (16) are read into
+// K loop. K advances in steps of BK = 64 (32 also compiles) through a ring of LDS stages
+// (two for the shipped configurations) filled straight from HBM by raw buffer loads
+// with an LDS destination (buffer_load_dwordx4 ... lds), so no register staging is
+// needed; the longer step halves the block barriers per flop, which is what the matrix
+// cores were waiting on. The buffer resources end at the tile's last valid row, so
+// ragged tiles read zeros without branches, and chunks beyond K are pointed past the end
+// to read zeros too. A stage row is BK bf16 = U = BK / 8 sixteen-byte units, unit u of
+// row r holding k-chunk u ^ ((r >> s) % U), with 2^s rows per 256 bytes, so that the
+// operand reads of 16 consecutive rows at one k-chunk hit distinct LDS banks; one load
+// instruction of a wave fills 1 KiB (64 / U rows), lane l writing unit l % U of row
+// l / U (the row's U lanes read its 2 BK contiguous bytes in permuted order). Within the loop the fragments of the next K slice (16) are read into
 // their own registers while the MFMAs of the current one run (scheduling groups put one
 // MFMA between consecutive loads and reads), across step boundaries too; the loop body
 // is branch-free (loads past the last step read zeros into spent
@@ -54,40 +55,48 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
-constexpr int kBK = 32;       // K step: one LDS stage row is 64 bytes
-constexpr int kSlices = kBK / 16;
 constexpr int kXcds = 8;
 constexpr int kGroupM = 8;
 constexpr uint32_t kBufferGDword3 = 0x00020000;  // raw 32-bit buffer, gfx9 family
 constexpr uint32_t kOutOfRange = 0x80000000u;    // beyond any resource's range: reads 0
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_ = 4>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_ = 4, int BK_ = 32>
 struct Tile {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_;
   static constexpr int kStages = STAGES_;   // LDS ring
+  static constexpr int BK = BK_;            // K step: a stage row is 2 BK bytes
+  static constexpr int kSlices = BK / 16;   // MFMA K slices per step
+  static constexpr int kUnits = BK / 8;     // 16-byte units per stage row
+  static constexpr int kRowsPerLoad = 64 / kUnits;            // rows one 1 KiB load fills
+  static constexpr int kSwzShift = BK == 32 ? 2 : 1;          // rows per 256 bytes: 4 or 2
+  static_assert(BK == 32 || BK == 64, "K step of 32 or 64");
   static constexpr int kWaves = WM * WN;
   static constexpr int kThreads = kWaves * kWave;
   static constexpr int TM = BM / WM / 32, TN = BN / WN / 32;   // MFMA tiles per wave
-  static constexpr int kStageElems = (BM + BN) * kBK;
+  static constexpr int kStageElems = (BM + BN) * BK;
   static constexpr int kEpiRow = BN + 8;                        // padded epilogue row
   static constexpr int kOperandElems = kStages * kStageElems;
   static constexpr int kLdsElems =
       (kOperandElems > BM * kEpiRow) ? kOperandElems : BM * kEpiRow;
-  static constexpr int kLA = BM / 16 / kWaves, kLB = BN / 16 / kWaves;  // loads per stage
+  static constexpr int kLA = BM / kRowsPerLoad / kWaves, kLB = BN / kRowsPerLoad / kWaves;
   static constexpr int kLoadsPerStage = kLA + kLB;
   static constexpr int kEpiThreadsPerRow = BN / 16;
   static constexpr int kEpiRowStep = kThreads / kEpiThreadsPerRow;
   static_assert(BM % (WM * 32) == 0 && BN % (WN * 32) == 0, "wave tiles are multiples of 32");
-  static_assert((BM / 16) % kWaves == 0 && (BN / 16) % kWaves == 0, "load blocks per wave");
+  static_assert((BM / kRowsPerLoad) % kWaves == 0 && (BN / kRowsPerLoad) % kWaves == 0,
+                "load blocks per wave");
   static_assert(kThreads % kEpiThreadsPerRow == 0, "epilogue mapping");
   static_assert(kLdsElems * 2 <= 160 * 1024, "LDS per block");
   static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerStage <= 63, "vector-memory counter range");
 };
 
 #ifndef LMBP_LIN_SMALL
-#define LMBP_LIN_SMALL 128, 128, 2, 2   // BM, BN, WM, WN of the small configuration
+#define LMBP_LIN_SMALL 128, 128, 2, 2, 2, 64   // the same for the small configuration
 #endif
-using BigTile = Tile<256, 256, 2, 4>;
+#ifndef LMBP_LIN_BIG
+#define LMBP_LIN_BIG 256, 256, 2, 4, 2, 64   // BM, BN, WM, WN, stages, K step: large configuration
+#endif
+using BigTile = Tile<LMBP_LIN_BIG>;
 using SmallTile = Tile<LMBP_LIN_SMALL>;
 
 // The target builtins below are wrapped in device functions: used directly in the body of
@@ -188,44 +197,52 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
   const auto rw = make_rsrc(w + n0 * K, rows_w * K * 2);
   const auto rw2 = make_rsrc(GLU ? a.w2 + n0 * K : w, GLU ? rows_w * K * 2 : 0);
 
-  // Loads: lane l of the wave's q-th 1 KiB block (rows 16 (wave + waves q) + l / 4)
-  // fetches k-chunk kc = (l % 4) ^ ((l / 16) & 3) of its row.
-  const int r_in = lane >> 2;
-  const int kc = (lane & 3) ^ ((r_in >> 2) & 3);
+  // Loads: lane l of the wave's q-th 1 KiB block (stage rows R (wave + waves q) + l / U,
+  // R rows of U units) fetches k-chunk kc = (l % U) ^ swz(row) of its row, so that unit u
+  // of stage row r holds chunk u ^ swz(r), swz(r) = (r >> kSwzShift) % U.
+  const int r_in = lane / C::kUnits;
+  const int u_in = lane % C::kUnits;
+  auto chunk = [&](int stage_row) { return u_in ^ ((stage_row >> C::kSwzShift) & (C::kUnits - 1)); };
   uint32_t ld_a[C::kLA], ld_b[C::kLB];  // byte offset of the chunk at K step 0
+  int kc_a[C::kLA], kc_b[C::kLB];
 #pragma unroll
-  for (int q = 0; q < C::kLA; ++q)
-    ld_a[q] = uint32_t(((wave + kWaves * q) * 16 + r_in) * K * 2 + kc * 16);
+  for (int q = 0; q < C::kLA; ++q) {
+    const int row = (wave + kWaves * q) * C::kRowsPerLoad + r_in;
+    kc_a[q] = chunk(row);
+    ld_a[q] = uint32_t(row * K * 2 + kc_a[q] * 16);
+  }
   // Gated form: B-tile rows below BN / 2 come from w, the others (the second half of the
   // loads, q >= kLB / 2) from w2, each at its own row offset.
 #pragma unroll
   for (int q = 0; q < C::kLB; ++q) {
-    const int row = (wave + kWaves * q) * 16 + r_in - ((GLU && q >= C::kLB / 2) ? BN / 2 : 0);
-    ld_b[q] = uint32_t(row * K * 2 + kc * 16);
+    const int srow = (wave + kWaves * q) * C::kRowsPerLoad + r_in;
+    kc_b[q] = chunk(srow);
+    const int row = srow - ((GLU && q >= C::kLB / 2) ? BN / 2 : 0);
+    ld_b[q] = uint32_t(row * K * 2 + kc_b[q] * 16);
   }
   constexpr int kStages = C::kStages;
   auto stage_ptr = [&](int64_t kt) { return lds + int(kt % kStages) * C::kStageElems; };
   auto issue_stage = [&](int64_t kt) {
     uint16_t* S = stage_ptr(kt);
-    const uint32_t k0b = uint32_t(kt * kBK * 2);
-    const bool kin = kt * kBK + kc * 8 < K;
+    const uint32_t k0b = uint32_t(kt * C::BK * 2);
 #pragma unroll
     for (int q = 0; q < C::kLA; ++q)
-      load_lds16(rx, S + (wave + kWaves * q) * 16 * kBK, kin ? ld_a[q] + k0b : kOutOfRange);
+      load_lds16(rx, S + (wave + kWaves * q) * 512,
+                 kt * C::BK + kc_a[q] * 8 < K ? ld_a[q] + k0b : kOutOfRange);
 #pragma unroll
     for (int q = 0; q < C::kLB; ++q)
-      load_lds16((GLU && q >= C::kLB / 2) ? rw2 : rw, S + BM * kBK + (wave + kWaves * q) * 16 * kBK,
-                 kin ? ld_b[q] + k0b : kOutOfRange);
+      load_lds16((GLU && q >= C::kLB / 2) ? rw2 : rw, S + BM * C::BK + (wave + kWaves * q) * 512,
+                 kt * C::BK + kc_b[q] * 8 < K ? ld_b[q] + k0b : kOutOfRange);
   };
 
   // Operand reads: lane l reads row (base + l % 32), k-chunk 2 kk + l / 32; wave rows
   // start at multiples of 32, so the row's swizzle is ((l % 32) >> 2) & 3.
-  const int swz = ((lane & 31) >> 2) & 3;
+  const int swz = ((lane & 31) >> C::kSwzShift) & (C::kUnits - 1);
   int a_row[TM], b_row[TN];
 #pragma unroll
-  for (int i = 0; i < TM; ++i) a_row[i] = (wm * TM * 32 + i * 32 + (lane & 31)) * kBK;
+  for (int i = 0; i < TM; ++i) a_row[i] = (wm * TM * 32 + i * 32 + (lane & 31)) * C::BK;
 #pragma unroll
-  for (int j = 0; j < TN; ++j) b_row[j] = BM * kBK + (wn * TN * 32 + j * 32 + (lane & 31)) * kBK;
+  for (int j = 0; j < TN; ++j) b_row[j] = BM * C::BK + (wn * TN * 32 + j * 32 + (lane & 31)) * C::BK;
   bf16x8 fa[2][TM], fb[2][TN];
   auto read = [&](const uint16_t* S, int kk, int buf) {
     const int unit = ((2 * kk + (lane >> 5)) ^ swz) * 8;
@@ -247,7 +264,7 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
   // constants (the vector-memory counter counts only these loads in the loop).
   constexpr int kPendingFirst = (kStages - 1) * C::kLoadsPerStage;    // loads after step 0
   constexpr int kPendingSteady = (kStages - 2) * C::kLoadsPerStage;   // after step kt + 1
-  const int64_t kt_count = (K + kBK - 1) / kBK;
+  const int64_t kt_count = (K + C::BK - 1) / C::BK;
   if (kt_count > 0) {
 #pragma unroll
     for (int s = 0; s < kStages; ++s) issue_stage(s);
@@ -257,8 +274,8 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
     for (int64_t kt = 0; kt + 1 < kt_count; ++kt) {
       const uint16_t* S = stage_ptr(kt);
 #pragma unroll
-      for (int kk = 0; kk < kSlices; ++kk) {
-        if (kk + 1 < kSlices) {
+      for (int kk = 0; kk < C::kSlices; ++kk) {
+        if (kk + 1 < C::kSlices) {
           read(S, kk + 1, (kk + 1) & 1);
           mfmas(kk & 1);
           spread<TM * TN, 0, TM + TN>();
@@ -278,8 +295,8 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
     }
     const uint16_t* S = stage_ptr(kt_count - 1);
 #pragma unroll
-    for (int kk = 0; kk < kSlices; ++kk) {
-      if (kk + 1 < kSlices) read(S, kk + 1, (kk + 1) & 1);
+    for (int kk = 0; kk < C::kSlices; ++kk) {
+      if (kk + 1 < C::kSlices) read(S, kk + 1, (kk + 1) & 1);
       __builtin_amdgcn_sched_barrier(0);
       mfmas(kk & 1);
     }
@@ -393,7 +410,8 @@ bool use_big_tiles(int64_t M, int64_t N_tile_cols) {
   int device = 0, cus = 256;
   if (hipGetDevice(&device) == hipSuccess)
     (void)hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device);
-  const int64_t big_tiles = ((M + 255) / 256) * ((N_tile_cols + 255) / 256);
+  const int64_t big_tiles = ((M + lin::BigTile::BM - 1) / lin::BigTile::BM) *
+                            ((N_tile_cols + lin::BigTile::BN - 1) / lin::BigTile::BN);
   return big_tiles >= int64_t(LMBP_LIN_BIG_MIN_ROUNDS) * cus;
 }
 }  // namespace
