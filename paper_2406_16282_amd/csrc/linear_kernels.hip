@@ -12,7 +12,7 @@
 // Tiling. A block computes a BM x BN tile of z with WM x WN waves, each a
 // (BM/WM) x (BN/WN) part as 32 x 32 MFMA tiles, accumulators in registers. Two tile
 // configurations are compiled and chosen per problem (launcher): 256 x 256 with 8 waves
-// of 128 x 64 for large problems, 128 x 128 with 4 waves of 64 x 64 (two blocks per CU)
+// of 128 x 64 for large problems, 128 x 128 with 8 waves of 64 x 32 (two blocks per CU)
 // when the large tiles would leave much of the last round of the GPU idle.
 //
 // K loop. K advances in steps of BK = 64 (32 also compiles) through a ring of LDS stages
@@ -91,7 +91,7 @@ struct Tile {
 };
 
 #ifndef LMBP_LIN_SMALL
-#define LMBP_LIN_SMALL 128, 128, 2, 2, 2, 64   // the same for the small configuration
+#define LMBP_LIN_SMALL 128, 128, 2, 4, 2, 64   // the same for the small configuration (8 waves)
 #endif
 #ifndef LMBP_LIN_BIG
 #define LMBP_LIN_BIG 256, 256, 2, 4, 2, 64   // BM, BN, WM, WN, stages, K step: large configuration
