@@ -212,24 +212,40 @@ def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
         nbwd = {"msrms": lmbp.msrms_bwd, "msln": lmbp.msln_bwd}[w.norm.op]
         afwd = {"resilu2": lmbp.resilu2_fwd, "regelu2": lmbp.regelu2_fwd}[w.act.op]
         abwd = {"resilu2": lmbp.resilu2_bwd, "regelu2": lmbp.regelu2_bwd}[w.act.op]
+        # SiLU workloads (the LLaMA MLP) also time the fused SwiGLU pair on the gate shape:
+        # u is the up projection, dy serves as dh; its codes are those of g, as above.
+        glu = w.act.op == "resilu2"
+        if glu:
+            gb = algorithmic_bytes(w, swiglu=True)
+            nb["reswiglu2_fwd"], nb["reswiglu2_bwd"] = gb["reswiglu2_fwd"], gb["reswiglu2_bwd"]
+            names = list(nb)
+            base = base + (T(w.act_u()),)
 
         def make_set(k):
             # Set k holds the block-0 tensors rotated by k * 4099 elements: same
             # values and distribution, distinct memory.
-            x, dz, g, dy = (t if k == 0 else torch.roll(t.view(-1), k * 4099).view_as(t) for t in base)
+            x, dz, g, dy, *rest = (t if k == 0 else torch.roll(t.view(-1), k * 4099).view_as(t) for t in base)
             st = {"x": x, "dz": dz, "g": g, "dy": dy, "z": torch.empty_like(x),
                   "rstd": torch.empty(w.norm.rows, dtype=torch.float32, device=dev),
                   "h": torch.empty_like(g), "dg": torch.empty_like(dy), "dx": torch.empty_like(dz),
                   "codes": torch.empty(lmbp.codes_words(g.numel()), dtype=torch.int32, device=dev)}
-            return [lambda: nfwd(st["x"], eps, z=st["z"], rstd=st["rstd"]),
-                    lambda: afwd(st["g"], y=st["h"], codes=st["codes"]),
-                    lambda: abwd(st["dy"], st["codes"], dx=st["dg"]),
-                    lambda: nbwd(st["dz"], st["z"], st["rstd"], dx=st["dx"])]
+            fns = [lambda: nfwd(st["x"], eps, z=st["z"], rstd=st["rstd"]),
+                   lambda: afwd(st["g"], y=st["h"], codes=st["codes"]),
+                   lambda: abwd(st["dy"], st["codes"], dx=st["dg"]),
+                   lambda: nbwd(st["dz"], st["z"], st["rstd"], dx=st["dx"])]
+            if glu:
+                st.update(u=rest[0], s=torch.empty_like(g), du=torch.empty_like(g))
+                fns += [lambda: lmbp.reswiglu2_fwd(st["g"], st["u"], h=st["h"], s=st["s"], codes=st["codes"]),
+                        lambda: lmbp.reswiglu2_bwd(st["dy"], st["u"], st["s"], st["codes"], dg=st["dg"],
+                                                   du=st["du"])]
+            return fns
 
         sets = [make_set(k) for k in range(nsets)]
         for ks in sets:
             ks[0]()
             ks[1]()
+            if glu:
+                ks[4]()
         torch.cuda.synchronize()
 
         def launch_us(i, order):
@@ -261,15 +277,19 @@ def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
         cold = {n: launch_us(i, bwd_order if n.endswith("_bwd") else fwd_order) for i, n in enumerate(names)}
         warm = {n: launch_us(i, [0]) for i, n in enumerate(names)}
         rec = {"sets": nsets, "set_bytes": set_bytes}
-        for pair, (f, b) in (("norm", (names[0], names[3])), ("act", (names[1], names[2]))):
+        pairs = [("norm", (names[0], names[3])), ("act", (names[1], names[2]))]
+        if glu:
+            pairs.append(("swiglu", (names[4], names[5])))
+        for pair, (f, b) in pairs:
             byt = nb[f] + nb[b]
             gbs = byt / ((cold[f] + cold[b]) * 1e-6) / 1e9
             rec[pair] = {"op": f[:-4], "fwd_us": round(cold[f], 2), "bwd_us": round(cold[b], 2),
                          "bytes": byt, "GBps": round(gbs, 1), "pct_of_peak": round(100 * gbs / HBM_PEAK_GBS, 1),
                          "warm_GBps": round(byt / ((warm[f] + warm[b]) * 1e-6) / 1e9, 1)}
         out[name] = rec
-        print(f"[bench] pairs {name}: norm {rec['norm']['GBps']} GB/s, act {rec['act']['GBps']} GB/s "
-              f"({nsets} sets)", file=sys.stderr, flush=True)
+        extra = f", swiglu {rec['swiglu']['GBps']} GB/s" if glu else ""
+        print(f"[bench] pairs {name}: norm {rec['norm']['GBps']} GB/s, act {rec['act']['GBps']} GB/s"
+              f"{extra} ({nsets} sets)", file=sys.stderr, flush=True)
         del sets, base
         torch.cuda.empty_cache()
     return out
