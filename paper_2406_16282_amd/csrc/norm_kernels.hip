@@ -7,9 +7,10 @@
 // Fast path: 1, 2 or 4 waves per row (chosen from the row width), the row held in
 // registers (thread t of a row holding 16-byte vectors t, t + 64*WPR, ...), so each
 // tensor is read from HBM once and every statistic is a register pass plus a wave
-// reduction (and one LDS exchange when a row spans several waves). Rows that are
-// not 16-byte aligned, or wider than 4 waves x 16 vectors, use a block-per-row path
-// that re-reads the row for each pass.
+// reduction (and one LDS exchange when a row spans several waves). The forward
+// for rows of one wave runs persistent blocks that prefetch their next row. Rows that
+// are not 16-byte aligned, or wider than 4 waves x 16 vectors, use a block-per-row
+// path that re-reads the row for each pass.
 //
 // Numerics: LN accumulates x - x0 (x0 = the row's first element) so that rows
 // with a large common offset do not lose the deviations to rounding; the centred
@@ -17,6 +18,8 @@
 // Variances are two-pass over the register-resident row.
 #include "lmbp_device.hpp"
 #include "lmbp_launch.hpp"
+
+#include <atomic>
 
 namespace lmbp {
 
@@ -206,6 +209,111 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_bwd_vec(const void* dz
   }
 }
 
+#ifndef LMBP_NORM_FWD_PIPE_WPR
+// The forward takes the persistent form below for rows of at most this many waves (0:
+// never). Measured: one wave per row (ViT-B, 768 wide) 11% faster; four waves per row
+// (LLaMA, 4096 and 5120 wide) 6% slower, and the backward slower in both cases.
+#define LMBP_NORM_FWD_PIPE_WPR 1
+#endif
+
+// Register-tile path, persistent form (forward): each block walks row groups
+// g = blockIdx.x, blockIdx.x + gridDim.x, ... (a group = the block's RPB rows), with the
+// next group's loads issued before the current group's reductions and stores, which
+// hides the load latency of short rows. Every access is a buffer instruction over the
+// row (an inactive row has an empty resource, padding lanes are out of range), so the
+// loop has no memory branches and the compiler waits only for the loads it needs. The
+// LDS slots alternate between consecutive groups: a wave can be at most one barrier
+// ahead of another.
+__device__ inline __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int64_t first_byte, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(static_cast<const char*>(base)) + first_byte, 0, bytes, 0x00020000);
+}
+constexpr uint32_t kNoLane = 0x80000000u;   // an offset beyond every resource
+
+template <class IO, bool LN, int VPL, int WPR>
+__global__ __launch_bounds__(norm_block<WPR>()) void norm_fwd_pipe(const void* x, void* z,
+                                                                   float* __restrict__ rstd,
+                                                                   int64_t rows, int cols, float eps) {
+  constexpr int E = IO::kPerVec;
+  constexpr int TPR = kWave * WPR;
+  constexpr int RPB = norm_block<WPR>() / TPR;
+  constexpr int kLoadPol = kFwdNtLoad ? 2 : 0;
+  __shared__ float red[2][2][norm_block<WPR>() / kWave];
+  const int t = threadIdx.x % TPR;
+  const int sub = wave_in_block() / WPR;
+  const int nv = cols / E;
+  const int64_t groups = (rows + RPB - 1) / RPB;
+
+  auto load = [&](int64_t g, u32x4 (&v)[VPL], float& pivot) {
+    const int64_t row = g * RPB + sub;
+    const bool active = g < groups && row < rows;
+    const auto r = row_rsrc(x, active ? row * nv * 16 : 0, active ? nv * 16 : 0);
+#pragma unroll
+    for (int j = 0; j < VPL; ++j)
+      v[j] = __builtin_amdgcn_raw_buffer_load_b128(r, uint32_t(j * TPR + t) * 16, 0, kLoadPol);
+    if constexpr (LN) {
+      float f[E];
+      IO::unpack(__builtin_amdgcn_raw_buffer_load_b128(r, 0, 0, kLoadPol), f);
+      pivot = f[0];
+    }
+  };
+
+  u32x4 v[VPL], vn[VPL];
+  float pivot = 0.0f, pivot_n = 0.0f;
+  int par = 0;
+  load(blockIdx.x, v, pivot);
+  for (int64_t g = blockIdx.x; g < groups; g += gridDim.x, par ^= 1) {
+    load(g + gridDim.x, vn, pivot_n);
+    const int64_t row = g * RPB + sub;
+    const bool active = row < rows;
+
+    float mean_d = 0.0f;
+    if constexpr (LN) {
+      float s[1] = {0.0f};
+#pragma unroll
+      for (int j = 0; j < VPL; ++j) {
+        float f[E];
+        IO::unpack(v[j], f);
+        const bool in = j * TPR + t < nv;
+#pragma unroll
+        for (int e = 0; e < E; ++e) s[0] += in ? f[e] - pivot : 0.0f;
+      }
+      row_sums<WPR>(s, &red[par][0]);
+      mean_d = s[0] / float(cols);
+    }
+    float q[1] = {0.0f};
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      float f[E];
+      IO::unpack(v[j], f);
+      const bool in = j * TPR + t < nv;
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const float c = in ? (LN ? (f[e] - pivot) - mean_d : f[e]) : 0.0f;
+        q[0] = __builtin_fmaf(c, c, q[0]);
+      }
+    }
+    row_sums<WPR>(q, &red[par][1]);
+    const float rs = rsqrtf(q[0] / float(cols) + eps);
+    const auto rz = row_rsrc(z, active ? row * nv * 16 : 0, active ? nv * 16 : 0);
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) {
+      opaque(v[j]);
+      float f[E];
+      IO::unpack(v[j], f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) f[e] = (LN ? (f[e] - pivot) - mean_d : f[e]) * rs;
+      __builtin_amdgcn_raw_buffer_store_b128(IO::pack(f), rz, uint32_t(j * TPR + t) * 16, 0,
+                                             LMBP_NORM_STORE_CPOL);
+    }
+    const auto rr = row_rsrc(rstd, active ? row * 4 : 0, active ? 4 : 0);
+    __builtin_amdgcn_raw_buffer_store_b32(__float_as_uint(rs), rr, t == 0 ? 0u : kNoLane, 0, 0);
+#pragma unroll
+    for (int j = 0; j < VPL; ++j) v[j] = vn[j];
+    pivot = pivot_n;
+  }
+}
+
 // Block per row, any alignment and width; each pass re-reads the row (from cache
 // for rows that fit).
 template <class IO, bool LN>
@@ -332,6 +440,28 @@ constexpr NormShape kShapes[] = {
     {8, 1}, {8, 2}, {8, 3}, {8, 4}, {8, 6}, {8, 8}};
 constexpr int kNumShapes = sizeof(kShapes) / sizeof(kShapes[0]);
 
+// Blocks of the persistent form: those resident at once on the device (from the
+// kernel's occupancy, queried once per kernel and device), at most one per row group.
+// Any grid is correct; if the queries fail, one block per group.
+template <auto Kernel>
+int64_t persistent_grid(int block, int64_t groups) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int64_t> resident[kMaxDevices];
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess || device < 0 || device >= kMaxDevices) return groups;
+  int64_t r = resident[device].load(std::memory_order_relaxed);
+  if (r == 0) {
+    int cus = 0, per_cu = 0;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess ||
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, Kernel, block, 0) != hipSuccess ||
+        cus <= 0 || per_cu <= 0)
+      return groups;
+    r = int64_t(cus) * per_cu;
+    resident[device].store(r, std::memory_order_relaxed);
+  }
+  return groups < r ? groups : r;
+}
+
 template <class IO, bool LN, int I>
 hipError_t fwd_dispatch(NormShape sh, int64_t rows, int cols, float eps, const void* x, void* z,
                         float* rstd, hipStream_t s) {
@@ -344,6 +474,12 @@ hipError_t fwd_dispatch(NormShape sh, int64_t rows, int cols, float eps, const v
         constexpr int rpb = norm_block<W>() / (kWave * W);
         const int64_t blocks = (rows + rpb - 1) / rpb;
         if (blocks > 0x7fffffff) return hipErrorInvalidValue;
+        if constexpr (W <= LMBP_NORM_FWD_PIPE_WPR) {
+          const int64_t grid = persistent_grid<norm_fwd_pipe<IO, LN, V, W>>(norm_block<W>(), blocks);
+          hipLaunchKernelGGL((norm_fwd_pipe<IO, LN, V, W>), dim3(unsigned(grid)), dim3(norm_block<W>()),
+                             0, s, x, z, rstd, rows, cols, eps);
+          return hipGetLastError();
+        }
         hipLaunchKernelGGL((norm_fwd_vec<IO, LN, V, W>), dim3(unsigned(blocks)), dim3(norm_block<W>()),
                            0, s, x, z, rstd, rows, cols, eps);
         return hipGetLastError();
