@@ -487,7 +487,8 @@ def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=200,
+                    help="untimed steps first; a few hundred bring the clocks to their steady state")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--swiglu", action="store_true",
                     help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
