@@ -295,6 +295,94 @@ def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
     return out
 
 
+def _graph_us(torch, fns, order, reps=48):
+    """Average duration (us) of one launch over `reps` launches of fns[k] for k cycling
+    through `order`, replayed from a HIP graph (launch-bound small kernels would
+    otherwise measure the host)."""
+    seq = [order[j % len(order)] for j in range(max(reps, len(order)))]
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for k in seq:
+            fns[k]()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for k in seq:
+            fns[k]()
+    graph.replay()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    graph.replay()
+    graph.replay()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) * 1e3 / (2 * len(seq))
+
+
+def variants_report(torch, lmbp, inputs, dev, cold_bytes=1 << 30):
+    """Forward + backward GB/s of the k-bit family kernels (stepact_fwd / stepact_bwd,
+    k = 1, 2, 3, 4, and ReGELU2-d) next to the dedicated k = 2 kernels, on the ViT-B
+    batch-64 GELU and LLaMA-7B gate SiLU activation shapes (bf16), cold: launches cycle
+    over enough tensor sets to touch 1 GiB, forwards in set order, backwards reversed.
+    Bytes per element: read x and write y (forward), read dy and write dx (backward),
+    plus the k-bit codes both ways (floor(32 / k) codes per 32-bit word)."""
+    from paper_2406_16282_amd import variants
+    shapes = {"vit_b_bs64_bf16": ("gelu", 64 * 197, 3072, 1.5),
+              "llama7b_gate_bf16": ("silu", 4 * 2048, 11008, 2.0)}
+    out = {}
+    for name, (act, rows, cols, std) in shapes.items():
+        n = rows * cols
+        x0 = inputs.storage_to_torch(inputs.normal((rows, cols), std, "bf16", tensor_id=2), dev)
+        dy0 = inputs.storage_to_torch(inputs.normal((rows, cols), 1e-2, "bf16", tensor_id=3), dev)
+        nsets = max(3, min(16, -(-cold_bytes // (4 * n))))
+        sets = [(x0, dy0) if k == 0 else (torch.roll(x0.view(-1), k * 4099).view_as(x0),
+                                          torch.roll(dy0.view(-1), k * 4099).view_as(dy0))
+                for k in range(nsets)]
+        outs = [(torch.empty_like(x0), torch.empty_like(x0)) for _ in range(nsets)]
+        members = []
+        span = 3.0 if act == "gelu" else 6.0
+        for bits in (1, 2, 3, 4):
+            m = (1 << bits) - 1
+            c = [span * (2 * i / (m - 1) - 1) if m > 1 else 0.0 for i in range(m)]
+            a = [1.0 / (m + 1)] * (m - 1)
+            members.append((f"k{bits}_even", bits, c, variants.levels_of(a)))
+        if act == "gelu":
+            members.append(("regelu2_d", 2, list(variants.REGELU2D_C), variants.levels_of(variants.REGELU2D_A)))
+        rec = {}
+        for label, bits, c, lv in members + [("dedicated_k2", 2, None, None)]:
+            words = int(lmbp.lib().lmbp_stepact_codes_bytes(bits, n)) // 4
+            codes = [torch.empty(words, dtype=torch.int32, device=dev) for _ in range(nsets)]
+            if c is None:
+                fwd_op = lmbp.regelu2_fwd if act == "gelu" else lmbp.resilu2_fwd
+                bwd_op = lmbp.regelu2_bwd if act == "gelu" else lmbp.resilu2_bwd
+                fwd = [lambda k=k: fwd_op(sets[k][0], y=outs[k][0], codes=codes[k]) for k in range(nsets)]
+                bwd = [lambda k=k: bwd_op(sets[k][1], codes[k], dx=outs[k][1]) for k in range(nsets)]
+            else:
+                fwd = [lambda k=k: lmbp.stepact_fwd(sets[k][0], act, c, bits, y=outs[k][0], codes=codes[k])
+                       for k in range(nsets)]
+                bwd = [lambda k=k: lmbp.stepact_bwd(sets[k][1], codes[k], lv, bits, dx=outs[k][1])
+                       for k in range(nsets)]
+            for f in fwd:
+                f()
+            torch.cuda.synchronize()
+            order = list(range(nsets))
+            tf = _graph_us(torch, fwd, order)
+            tb = _graph_us(torch, bwd, order[::-1])
+            byt = 2 * (2 * 2 * n + 4 * words)
+            rec[label] = {"bits": bits, "stored_bits_per_elt": round(32 * words / n, 3),
+                          "fwd_us": round(tf, 2), "bwd_us": round(tb, 2), "bytes": byt,
+                          "GBps": round(byt / ((tf + tb) * 1e-6) / 1e9, 1),
+                          "pct_of_peak": round(100 * byt / ((tf + tb) * 1e-6) / 1e9 / HBM_PEAK_GBS, 1)}
+            del codes
+        out[name] = rec
+        print(f"[bench] variants {name}: " + ", ".join(f"{k} {v['GBps']}" for k, v in rec.items()),
+              file=sys.stderr, flush=True)
+        del sets, outs
+        torch.cuda.empty_cache()
+    return out
+
+
 MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak, AMD published
 
 LINEAR_SHAPES = {
@@ -497,6 +585,9 @@ def main():
     ap.add_argument("--blocks", action="store_true",
                     help="also report the training step time and kept activation memory of whole "
                          "ViT-B and LLaMA-7B MLP blocks, torch modules against this library's")
+    ap.add_argument("--variants", action="store_true",
+                    help="also report the k-bit family kernels (k = 1..4, ReGELU2-d) against the "
+                         "dedicated k = 2 kernels")
     ap.add_argument("--linear", action="store_true",
                     help="also report the fused linear + activation forward against the unfused "
                          "library GEMM + activation kernel")
@@ -708,6 +799,9 @@ def main():
     if args.linear:
         print("[bench] fused linear + activation", file=sys.stderr, flush=True)
         out["linear"] = linear_report(torch, lmbp, inputs, dev, reps=max(10, min(args.steps, 50)))
+    if args.variants:
+        print("[bench] k-bit family", file=sys.stderr, flush=True)
+        out["variants"] = variants_report(torch, lmbp, inputs, dev)
     if args.blocks:
         print("[bench] MLP blocks", file=sys.stderr, flush=True)
         out["blocks"] = block_report(torch, dev, reps=max(5, min(args.steps, 20)))
