@@ -12,11 +12,12 @@
 // and OR them together with cross-lane shuffles, and the group's first lane stores the
 // word.
 //
+// Codes are counted by a linear pass over the thresholds for k <= 2 and by binary search
+// over an LDS copy of the table for k = 3, 4.
+//
 // k = 3: ten codes per word (bits 3j .. 3j + 2, top two bits zero), so a word's codes
-// do not fall on vector boundaries. A wave handles 640 elements (64 words): each lane
-// converts whole vectors and writes their codes as bytes to the wave's LDS area, then
-// lane l packs bytes 10 l .. 10 l + 9 into word l (coalesced stores). The backward
-// stages the 64 words in LDS the same way and each element reads its 3 bits there.
+// do not fall on vector boundaries; five vectors are whole words, and the k = 3 kernels
+// below tile by them.
 #include "lmbp_device.hpp"
 #include "act_math.hpp"
 #include "lmbp_launch.hpp"
@@ -43,6 +44,19 @@ __device__ inline uint32_t count_below(float x, const StepTable& tab) {
   return c;
 }
 
+// The same count by binary search over the increasing thresholds (duplicates, which
+// the round-down can produce, are counted alike): the first probe is the middle
+// threshold, a kernel argument; the others read the lane's own entry of an LDS copy of
+// the table. k - 1 LDS reads per element instead of 2^k - 1 compares.
+template <int BITS>
+__device__ inline uint32_t search_below(float x, const StepTable& tab, const float* lt) {
+  constexpr uint32_t H = 1u << (BITS - 1);
+  uint32_t c = (x > tab.t[H - 1]) ? H : 0u;
+#pragma unroll
+  for (uint32_t step = H / 2; step >= 1; step /= 2) c += (x > lt[c + step - 1]) ? step : 0u;
+  return c;
+}
+
 template <int G>
 __device__ inline uint32_t group_or(uint32_t v) {
 #pragma unroll
@@ -57,6 +71,16 @@ __global__ __launch_bounds__(128) void stepact_fwd_kernel(const void* x, void* y
   using S = StepShape<IO, BITS>;
   constexpr bool kPrecise = std::is_same<IO, F32>::value;
   constexpr int E = S::E;
+  constexpr bool kSearch = BITS >= 3;
+  __shared__ float lt[16];
+  if constexpr (kSearch) {
+    if (threadIdx.x < S::NT) lt[threadIdx.x] = tab.t[threadIdx.x];
+    __syncthreads();
+  }
+  auto code = [&](float v) {
+    if constexpr (kSearch) return search_below<BITS>(v, tab, lt);
+    else return count_below<S::NT>(v, tab);
+  };
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t wave = int64_t(blockIdx.x) * (blockDim.x / kWave) + (threadIdx.x / kWave);
   const int64_t base = wave * S::TILE;
@@ -70,7 +94,7 @@ __global__ __launch_bounds__(128) void stepact_fwd_kernel(const void* x, void* y
 #pragma unroll
     for (int e = 0; e < E; ++e) {
       o[e] = act_value<ACT, kPrecise>(f[e]);
-      part |= count_below<S::NT>(f[e], tab) << (BITS * e);
+      part |= code(f[e]) << (BITS * e);
     }
     stg16<true>(y, base / E + lane, IO::pack(o));
     const uint32_t word = group_or<S::G>(S::G == 1 ? part : part << ((lane % S::G) * S::PART));
@@ -89,7 +113,7 @@ __global__ __launch_bounds__(128) void stepact_fwd_kernel(const void* x, void* y
       if (i < n) {
         const float xv = IO::load1(x, i);
         IO::store1(y, i, act_value<ACT, kPrecise>(xv));
-        word |= count_below<S::NT>(xv, tab) << (BITS * e);
+        word |= code(xv) << (BITS * e);
       }
     }
     codes[w] = word;
@@ -132,45 +156,93 @@ __global__ __launch_bounds__(128) void stepact_bwd_kernel(const void* dy,
 }
 
 // ------------------------------------------------------------------ k = 3
-constexpr int kTile3 = 640;     // elements per wave: 64 words of 10 codes
-constexpr int kWords3 = kTile3 / 10;
+// Ten codes per word: 5 vectors (5 E elements) are E / 2 whole words. A wave tile is 64 x 5
+// vectors. Forward, phase 1 (coalesced, vector j * 64 + lane): activation, y stored, and
+// the vector's E codes as one 3E-bit part written to the wave's LDS area; phase 2: lane l
+// reads the parts of vectors 5 l .. 5 l + 4 (odd stride: no bank conflicts), which are
+// exactly words (E / 2) l .. (E / 2) l + E / 2 - 1, and stores them with one vector store.
+// Backward: the tile's words are staged in LDS, and a vector's 3E code bits, which start
+// at bit 3 (vE mod 10) of word vE / 10 and may run into the next word, come from two reads.
+constexpr int kVec3 = 5;
+
+template <class IO>
+struct Tile3 {
+  static constexpr int E = IO::kPerVec;
+  static constexpr int TILE = kWave * kVec3 * E;   // elements per wave tile
+  static constexpr int WPL = kVec3 * E / 10;       // code words per lane
+  static constexpr int WORDS = kWave * WPL;        // code words per wave tile
+  static constexpr int PART = 3 * E;               // code bits per vector
+};
+
+// Word i (30 bits) of the concatenation of the 5 parts (part j at bit PART j).
+template <int PART, int I>
+__device__ inline uint32_t word_of_parts(const uint32_t (&p)[kVec3]) {
+  uint32_t w = 0;
+#pragma unroll
+  for (int j = 0; j < kVec3; ++j) {
+    const int sh = PART * j - 30 * I;   // position of part j relative to the word's bit 0
+    if (sh > -PART && sh < 30) w |= sh >= 0 ? p[j] << sh : p[j] >> -sh;
+  }
+  return w & 0x3FFFFFFFu;
+}
 
 template <class IO, int ACT>
 __global__ __launch_bounds__(128) void stepact3_fwd_kernel(const void* x, void* y,
                                                            uint32_t* __restrict__ codes, int64_t n,
                                                            int vec_ok, StepTable tab) {
+  using T3 = Tile3<IO>;
   constexpr bool kPrecise = std::is_same<IO, F32>::value;
-  constexpr int E = IO::kPerVec;
-  constexpr int NV = kTile3 / E;   // vectors per wave tile
-  __shared__ uint8_t lcodes[2][kTile3];
+  constexpr int E = T3::E;
+  __shared__ float lt[8];
+  __shared__ uint32_t lparts[2][kWave * kVec3];
+  if (threadIdx.x < 7) lt[threadIdx.x] = tab.t[threadIdx.x];
+  __syncthreads();
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
-  const int64_t base = (int64_t(blockIdx.x) * 2 + wv) * kTile3;
+  const int64_t base = (int64_t(blockIdx.x) * 2 + wv) * T3::TILE;
   if (base >= n) return;
 
-  if (vec_ok && base + kTile3 <= n) {
-    uint8_t* lc = lcodes[wv];
-    for (int v = lane; v < NV; v += kWave) {
+  if (vec_ok && base + T3::TILE <= n) {
+    uint32_t* lp = lparts[wv];
+#pragma unroll
+    for (int j = 0; j < kVec3; ++j) {
+      const int v = j * kWave + lane;
       const u32x4 in = ldg16<true>(x, base / E + v);
       float f[E], o[E];
       IO::unpack(in, f);
+      uint32_t part = 0;
 #pragma unroll
       for (int e = 0; e < E; ++e) {
         o[e] = act_value<ACT, kPrecise>(f[e]);
-        lc[v * E + e] = uint8_t(count_below<7>(f[e], tab));
+        part |= search_below<3>(f[e], tab, lt) << (3 * e);
       }
       stg16<true>(y, base / E + v, IO::pack(o));
+      lp[v] = part;
     }
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // every lane's bytes are in LDS
-    uint32_t word = 0;
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the wave's parts are in LDS
+    uint32_t p[kVec3];
 #pragma unroll
-    for (int j = 0; j < 10; ++j) word |= uint32_t(lc[lane * 10 + j]) << (3 * j);
-    codes[base / 10 + lane] = word;
+    for (int j = 0; j < kVec3; ++j) p[j] = lp[kVec3 * lane + j];
+    uint32_t* cw = codes + base / 10 + T3::WPL * lane;
+    if constexpr (T3::WPL == 4) {
+      u32x4 w;
+      w[0] = word_of_parts<T3::PART, 0>(p);
+      w[1] = word_of_parts<T3::PART, 1>(p);
+      w[2] = word_of_parts<T3::PART, 2>(p);
+      w[3] = word_of_parts<T3::PART, 3>(p);
+      *reinterpret_cast<u32x4*>(cw) = w;
+    } else {
+      static_assert(T3::WPL == 2, "fp32: two words per lane");
+      uint2 w;
+      w.x = word_of_parts<T3::PART, 0>(p);
+      w.y = word_of_parts<T3::PART, 1>(p);
+      *reinterpret_cast<uint2*>(cw) = w;
+    }
     return;
   }
 
   // General path: partial last tile or unaligned pointers; one code word per lane.
-  const int64_t end = (base + kTile3 < n) ? base + kTile3 : n;
+  const int64_t end = (base + T3::TILE < n) ? base + T3::TILE : n;
   const int64_t w_end = (end + 9) / 10;
   for (int64_t w = base / 10 + lane; w < w_end; w += kWave) {
     uint32_t word = 0;
@@ -179,7 +251,7 @@ __global__ __launch_bounds__(128) void stepact3_fwd_kernel(const void* x, void* 
       if (i < n) {
         const float xv = IO::load1(x, i);
         IO::store1(y, i, act_value<ACT, kPrecise>(xv));
-        word |= count_below<7>(xv, tab) << (3 * j);
+        word |= search_below<3>(xv, tab, lt) << (3 * j);
       }
     }
     codes[w] = word;
@@ -191,35 +263,45 @@ __global__ __launch_bounds__(128) void stepact3_bwd_kernel(const void* dy,
                                                            const uint32_t* __restrict__ codes,
                                                            void* dx, int64_t n, int vec_ok,
                                                            StepTable tab) {
-  constexpr int E = IO::kPerVec;
-  constexpr int NV = kTile3 / E;
+  using T3 = Tile3<IO>;
+  constexpr int E = T3::E;
   __shared__ float lv[8];
-  __shared__ uint32_t lwords[2][kWords3];
+  __shared__ uint32_t lwords[2][T3::WORDS + 1];
   if (threadIdx.x < 8) lv[threadIdx.x] = tab.lv[threadIdx.x];
   __syncthreads();
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
-  const int64_t base = (int64_t(blockIdx.x) * 2 + wv) * kTile3;
+  const int64_t base = (int64_t(blockIdx.x) * 2 + wv) * T3::TILE;
   if (base >= n) return;
 
-  if (vec_ok && base + kTile3 <= n) {
-    uint32_t* lw = lwords[wv];
-    lw[lane] = codes[base / 10 + lane];
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // every lane's word is in LDS
-    for (int v = lane; v < NV; v += kWave) {
-      float f[E];
-      IO::unpack(ldg16<true>(dy, base / E + v), f);
+  if (vec_ok && base + T3::TILE <= n) {
+    // The gradient vectors are requested first, so their latency overlaps the staging of
+    // the code words.
+    u32x4 g[kVec3];
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        const int i = v * E + e;
-        f[e] *= lv[(lw[i / 10] >> (3 * (i % 10))) & 7u];
-      }
+    for (int j = 0; j < kVec3; ++j) g[j] = ldg16<true>(dy, base / E + j * kWave + lane);
+    uint32_t* lw = lwords[wv];
+#pragma unroll
+    for (int i = 0; i < T3::WPL; ++i) lw[i * kWave + lane] = codes[base / 10 + i * kWave + lane];
+    if (lane == 0) lw[T3::WORDS] = 0u;   // read (and discarded) by the last vector
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");   // the tile's words are in LDS
+#pragma unroll
+    for (int j = 0; j < kVec3; ++j) {
+      const int v = j * kWave + lane;
+      const int first = v * E;              // element offset in the tile
+      const int w0 = first / 10, o = first % 10;
+      const uint64_t pair = (uint64_t(lw[w0 + 1]) << 30) | (lw[w0] & 0x3FFFFFFFu);
+      const uint32_t bits = uint32_t(pair >> (3 * o));
+      float f[E];
+      IO::unpack(g[j], f);
+#pragma unroll
+      for (int e = 0; e < E; ++e) f[e] *= lv[(bits >> (3 * e)) & 7u];
       stg16<true>(dx, base / E + v, IO::pack(f));
     }
     return;
   }
 
-  const int64_t end = (base + kTile3 < n) ? base + kTile3 : n;
+  const int64_t end = (base + T3::TILE < n) ? base + T3::TILE : n;
   for (int64_t i = base + lane; i < end; i += kWave) {
     const uint32_t c = (codes[i / 10] >> (3 * (i % 10))) & 7u;
     IO::store1(dx, i, IO::load1(dy, i) * lv[c]);
@@ -227,15 +309,16 @@ __global__ __launch_bounds__(128) void stepact3_bwd_kernel(const void* dy,
 }
 
 namespace {
+template <class IO>
 int64_t step3_blocks(int64_t n) {
-  const int64_t waves = (n + kTile3 - 1) / kTile3;
+  const int64_t waves = (n + Tile3<IO>::TILE - 1) / Tile3<IO>::TILE;
   return (waves + 1) / 2;  // 2 waves per 128-thread block
 }
 
 template <class IO, int ACT>
 hipError_t fwd3(int64_t n, const void* x, void* y, uint32_t* codes, bool vec_ok,
                 const StepTable& tab, hipStream_t s) {
-  const int64_t blocks = step3_blocks(n);
+  const int64_t blocks = step3_blocks<IO>(n);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((stepact3_fwd_kernel<IO, ACT>), dim3(unsigned(blocks)), dim3(128), 0, s, x, y,
                      codes, n, int(vec_ok), tab);
@@ -245,7 +328,7 @@ hipError_t fwd3(int64_t n, const void* x, void* y, uint32_t* codes, bool vec_ok,
 template <class IO>
 hipError_t bwd3(int64_t n, const void* dy, const uint32_t* codes, void* dx, bool vec_ok,
                 const StepTable& tab, hipStream_t s) {
-  const int64_t blocks = step3_blocks(n);
+  const int64_t blocks = step3_blocks<IO>(n);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
   hipLaunchKernelGGL((stepact3_bwd_kernel<IO>), dim3(unsigned(blocks)), dim3(128), 0, s, dy, codes,
                      dx, n, int(vec_ok), tab);
