@@ -1,0 +1,38 @@
+"""bench.py on the GPU, run as its own process with a short step count: it prints one
+JSON line with the fields of the benchmark contract, and its numbers agree with each
+other (value = bytes per step / step time; the roofline fraction = achieved / peak)."""
+
+import json
+import os
+import subprocess
+import sys
+
+import pytest
+
+pytestmark = pytest.mark.gpu
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.mark.parametrize("flags", [[], ["--swiglu"]], ids=["plain", "swiglu"])
+def test_bench_prints_one_contract_line(flags):
+    print(f"[bench contract] bench.py --steps 5 --warmup 5 --no-cpu-baseline {' '.join(flags)}", flush=True)
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "5", "--warmup", "5",
+                        "--no-cpu-baseline", *flags],
+                       capture_output=True, text=True, timeout=110, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    lines = [l for l in r.stdout.splitlines() if l.strip()]
+    assert len(lines) == 1, r.stdout
+    d = json.loads(lines[0])
+    for key in ("metric", "value", "unit", "n_gpus", "steps", "warmup", "ms_per_step", "higher_is_better",
+                "scaling", "vs_baseline", "dtype", "data", "config", "roofline"):
+        assert key in d, key
+    assert d["n_gpus"] == 1 and d["steps"] == 5 and d["warmup"] == 5
+    assert d["unit"] == "GB/s" and d["higher_is_better"] is True and d["data"] == "synthetic"
+    assert "workload" in d["config"]
+    step_bytes = d["config"]["bytes_per_step"]
+    assert d["value"] == pytest.approx(step_bytes / (d["ms_per_step"] * 1e-3) / 1e9, rel=2e-3)
+    rf = d["roofline"]
+    assert rf["bound"] == "hbm" and rf["unit"] == "GB/s" and rf["peak"] == 8000.0
+    assert rf["frac"] == pytest.approx(rf["achieved"] / rf["peak"], abs=1e-4)
+    assert 0.3 < rf["frac"] < 1.0
+    assert set(d["per_kernel"]) == {rf["kernel"]} | set(d["per_kernel"])
