@@ -35,4 +35,4 @@ def test_bench_prints_one_contract_line(flags):
     assert rf["bound"] == "hbm" and rf["unit"] == "GB/s" and rf["peak"] == 8000.0
     assert rf["frac"] == pytest.approx(rf["achieved"] / rf["peak"], abs=1e-4)
     assert 0.3 < rf["frac"] < 1.0
-    assert set(d["per_kernel"]) == {rf["kernel"]} | set(d["per_kernel"])
+    assert rf["kernel"] in d["per_kernel"]
