@@ -18,15 +18,31 @@ def T(a):
     return inputs.storage_to_torch(a, DEV)
 
 
+# k-bit family tables for k = 3 and 4 (evenly spaced biases; any increasing table will do).
+_C3 = [-2.0 + i * (4.0 / 6) for i in range(7)]
+_L3 = [i / 7 for i in range(8)]
+_C4 = [-3.0 + i * (6.0 / 14) for i in range(15)]
+_L4 = [i / 15 for i in range(16)]
+
+
 def _step(t, out):
-    """MS-RMSNorm fwd, ReSiLU2 fwd, ReSiLU2 bwd, MS-RMSNorm bwd, and the fused pair,
-    writing into the preallocated ``out`` tensors on the current stream."""
+    """MS-RMSNorm and MS-LN fwd / bwd, ReSiLU2 fwd / bwd, the fused SwiGLU pair, the
+    k = 3 and k = 4 family kernels and (bf16) the fused linear layer, writing into the
+    preallocated ``out`` tensors on the current stream."""
     lmbp.msrms_fwd(t["x"], 1e-5, z=out["z"], rstd=out["rstd"])
     lmbp.resilu2_fwd(t["g"], y=out["y"], codes=out["codes"])
     lmbp.resilu2_bwd(t["dy"], out["codes"], dx=out["dg"])
     lmbp.msrms_bwd(t["dz"], out["z"], out["rstd"], dx=out["dx"])
     lmbp.reswiglu2_fwd(t["g"], t["u"], h=out["h"], s=out["s"], codes=out["codes2"])
     lmbp.reswiglu2_bwd(t["dy"], t["u"], out["s"], out["codes2"], dg=out["dg2"], du=out["du2"])
+    lmbp.msln_fwd(t["x"], 1e-6, z=out["zl"], rstd=out["rstdl"])
+    lmbp.msln_bwd(t["dz"], out["zl"], out["rstdl"], dx=out["dxl"])
+    lmbp.stepact_fwd(t["g"], "gelu", _C3, 3, y=out["y3"], codes=out["codes3"])
+    lmbp.stepact_bwd(t["dy"], out["codes3"], _L3, 3, dx=out["dx3"])
+    lmbp.stepact_fwd(t["g"], "silu", _C4, 4, y=out["y4"], codes=out["codes4"])
+    lmbp.stepact_bwd(t["dy"], out["codes4"], _L4, 4, dx=out["dx4"])
+    if t["x"].dtype == torch.bfloat16:
+        lmbp.linear_act_fwd(t["x"], t["w"], t["b"], act="gelu", y=out["yl"], codes=out["codesl"])
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
@@ -37,14 +53,24 @@ def test_graph_replay_matches_eager(dtype):
          "g": T(inputs.normal((rows, f), 2.0, dtype, tensor_id=inputs.ACT_X)),
          "dy": T(inputs.normal((rows, f), 1.0, dtype, tensor_id=inputs.ACT_DY)),
          "u": T(inputs.normal((rows, f), 1.0, dtype, tensor_id=inputs.ACT_U))}
+    if dtype == "bf16":
+        t["w"] = T(inputs.normal((f, p), p ** -0.5, "bf16", tensor_id=inputs.LIN_W))
+        t["b"] = T(inputs.normal((f,), 0.1, "bf16", tensor_id=inputs.LIN_B))
 
     def alloc():
         e = lambda like: torch.empty_like(like)
-        return {"z": e(t["x"]), "rstd": torch.empty(rows, dtype=torch.float32, device=DEV),
-                "y": e(t["g"]), "codes": torch.empty(lmbp.codes_words(rows * f), dtype=torch.int32, device=DEV),
-                "dg": e(t["g"]), "dx": e(t["x"]), "h": e(t["g"]), "s": e(t["g"]),
-                "codes2": torch.empty(lmbp.codes_words(rows * f), dtype=torch.int32, device=DEV),
-                "dg2": e(t["g"]), "du2": e(t["g"])}
+        o = {"z": e(t["x"]), "rstd": torch.empty(rows, dtype=torch.float32, device=DEV),
+             "y": e(t["g"]), "codes": torch.empty(lmbp.codes_words(rows * f), dtype=torch.int32, device=DEV),
+             "dg": e(t["g"]), "dx": e(t["x"]), "h": e(t["g"]), "s": e(t["g"]),
+             "codes2": torch.empty(lmbp.codes_words(rows * f), dtype=torch.int32, device=DEV),
+             "dg2": e(t["g"]), "du2": e(t["g"]), "zl": e(t["x"]),
+             "rstdl": torch.empty(rows, dtype=torch.float32, device=DEV), "dxl": e(t["x"]),
+             "y3": e(t["g"]), "dx3": e(t["g"]), "y4": e(t["g"]), "dx4": e(t["g"]),
+             "codes3": torch.empty(-(-rows * f // 10), dtype=torch.int32, device=DEV),
+             "codes4": torch.empty(-(-rows * f // 8), dtype=torch.int32, device=DEV)}
+        if dtype == "bf16":   # the fused linear layer is bf16 only
+            o.update(yl=e(t["g"]), codesl=torch.empty(lmbp.codes_words(rows * f), dtype=torch.int32, device=DEV))
+        return o
 
     eager = alloc()
     _step(t, eager)
