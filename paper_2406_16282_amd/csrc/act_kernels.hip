@@ -9,7 +9,9 @@
 // vector index tile_vec + j*64 + l, so every load and store instruction of the
 // wave covers 1 KiB of contiguous memory. A vector carries 4 (fp32) or 8 (bf16)
 // elements, i.e. 8 or 16 code bits; G = 4 or 2 neighbouring lanes hold the parts
-// of one code word. Each lane packs its G parts for G consecutive vectors into one
+// of one code word. With one vector per lane (fp32, and the bf16 SwiGLU kernels) the
+// G lanes of a group shift their parts into place and OR them; with VPL a multiple of
+// G, each lane packs its G parts for G consecutive vectors into one
 // 32-bit value and the group transposes them with DPP quad permutes, after which
 // lane q of a group owns the complete word of vector (G*m + q): the word stores of
 // a wave are then contiguous too.
@@ -19,8 +21,9 @@
 #include "lmbp_launch.hpp"
 
 #ifndef LMBP_ACT_VPL
-// 16-byte vectors per lane in one wave tile (fp32 uses at least 4: one code word
-// spans 4 lanes). Small tiles mean many short-lived waves, which measured best.
+// 16-byte vectors per lane in one wave tile, bf16 storage (1, or a multiple of the 2
+// lanes that share a code word). Small tiles mean many short-lived waves, which
+// measured best; one vector was 2-6% slower.
 #define LMBP_ACT_VPL 2
 #endif
 #ifndef LMBP_ACT_VPL_F32
