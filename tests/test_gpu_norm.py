@@ -82,6 +82,18 @@ SHAPE_WIDTHS = {"bf16": [512, 1024, 2048, 4096, 5120, 8192, 12288, 16384, 24576,
 
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 @pytest.mark.parametrize("op", ["msln", "msrms"])
+def test_forward_row_groups_walked_by_persistent_blocks(op, dtype):
+    """Rows of one wave (here 512 wide) take the persistent forward: with many more row
+    groups than resident blocks, each block walks several groups with the next one's loads
+    in flight and alternating LDS slots; the row count leaves the last group partial."""
+    rows, cols = 24003, 512
+    x = inputs.normal((rows, cols), 1.0, dtype, tensor_id=inputs.NORM_X, block=11)
+    dz = inputs.normal((rows, cols), 1.0, dtype, tensor_id=inputs.NORM_DZ, block=11)
+    check_norm(op, dtype, x, dz, 1e-5, f"persistent({rows}x{cols})")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp32"])
+@pytest.mark.parametrize("op", ["msln", "msrms"])
 def test_every_launch_shape(op, dtype):
     for k, cols in enumerate(SHAPE_WIDTHS[dtype]):
         rows = 7  # not a multiple of the rows per block: the last block has idle rows
