@@ -86,10 +86,10 @@ def source_hash():
     return h.hexdigest()
 
 
-def load_traffic(kernel):
-    """HBM traffic of `kernel` from committed hardware-counter summaries, or None when
-    there is none or the kernel sources changed since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{WORKLOAD}.json")
+def load_traffic(kernel, workload=WORKLOAD):
+    """HBM traffic of `kernel` on `workload` from committed hardware-counter summaries, or
+    None when there is none or the kernel sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -583,6 +583,9 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=200,
                     help="untimed steps first; a few hundred bring the clocks to their steady state")
+    ap.add_argument("--workload", default=WORKLOAD,
+                    help="the step's tensors (a name from inputs.WORKLOADS; the default is the "
+                         "LLaMA-7B-shaped configuration the metric is quoted on)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--swiglu", action="store_true",
                     help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
@@ -608,12 +611,18 @@ def main():
 
     from paper_2406_16282_amd import inputs
 
+    wl = args.workload
+    if wl not in inputs.WORKLOADS:
+        sys.exit(f"--workload must be one of {', '.join(inputs.WORKLOADS)}")
+    if args.swiglu and inputs.WORKLOADS[wl].act.op != "resilu2":
+        sys.exit("--swiglu needs a SiLU workload")
+
     # The CPU oracle runs first: its worker processes start from a process that has not
     # touched the GPU yet.
     cpu = {}
     if not args.no_cpu_baseline and not args.swiglu:
         print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
-        w0 = inputs.WORKLOADS[WORKLOAD]
+        w0 = inputs.WORKLOADS[wl]
         tensors = (w0.norm_x(), w0.norm_dz(), w0.act_x(), w0.act_dy())
         cpu["cpu_baseline"] = cpu_baseline(w0, tensors)
         procs = max(1, min(16, os.cpu_count() or 1))
@@ -627,10 +636,10 @@ def main():
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
     dev = torch.device("cuda:0")
-    w = inputs.WORKLOADS[WORKLOAD]
+    w = inputs.WORKLOADS[wl]
     nb = algorithmic_bytes(w, args.swiglu)
     eps = float(np.float32(w.norm.eps))
-    print(f"[bench] generating {WORKLOAD} inputs", file=sys.stderr, flush=True)
+    print(f"[bench] generating {wl} inputs", file=sys.stderr, flush=True)
     T = lambda a: inputs.storage_to_torch(a, dev)
     x, dz, g, dy = T(w.norm_x()), T(w.norm_dz()), T(w.act_x()), T(w.act_dy())
     u = T(w.act_u()) if args.swiglu else None
@@ -763,7 +772,7 @@ def main():
         "dtype": "f32",
         "data": "synthetic",
         "config": {
-            "workload": WORKLOAD + ("_fused" if args.swiglu else ""),
+            "workload": wl + ("_fused" if args.swiglu else ""),
             "storage": w.act.dtype,
             "norm": f"{w.norm.op} [{w.norm.rows}x{w.norm.cols}] eps={w.norm.eps:g}",
             "act": (f"reswiglu2 (SiLU(g) * u) [{w.act.rows}x{w.act.cols}]" if args.swiglu
@@ -786,7 +795,7 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": load_traffic(dominant + ("_fused" if args.swiglu else "")),
+            "traffic": load_traffic(dominant + ("_fused" if args.swiglu else ""), wl),
         },
         "copy_reference": {"bytes_moved": 2 * copy_bytes, "us": round(copy_ms * 1e3, 2),
                            "GBps": round(2 * copy_bytes / (copy_ms * 1e-3) / 1e9, 1)},

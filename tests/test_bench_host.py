@@ -51,3 +51,9 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120, cwd=ROOT)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_unknown_workload_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "no_such_shape",
+                        "--no-cpu-baseline"], capture_output=True, text=True, timeout=120, cwd=ROOT)
+    assert r.returncode != 0 and "--workload must be one of" in r.stderr and r.stdout == ""
