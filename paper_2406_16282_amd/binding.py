@@ -7,6 +7,7 @@ in the library's HIP kernels. There is no fallback: if liblmbp.so has not been
 built, the first call raises.
 """
 
+import contextlib
 import ctypes
 import math
 import os
@@ -132,16 +133,31 @@ def _on(t, ref, what):
     return t
 
 
+# torch's own accessor of the current stream's raw handle (a few hundred ns, against ~2 us
+# for building a torch.cuda.Stream object); the public call is the fallback.
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(t, stream):
     """The HIP stream to launch on: the tensors' current stream by default, else a
     torch.cuda.Stream of the same device or a raw stream handle."""
     if stream is None:
+        if _raw_stream is not None:
+            return ctypes.c_void_p(_raw_stream(t.device.index))
         return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
     if isinstance(stream, torch.cuda.Stream):
         if stream.device != t.device:
             raise ValueError(f"stream is on {stream.device}, the tensors on {t.device}")
         return ctypes.c_void_p(stream.cuda_stream)
     return ctypes.c_void_p(int(stream))
+
+
+def _device_of(t):
+    """Launches go to the tensors' GPU: a no-op context when it is already the current
+    device (the common case; switching costs ~1.5 us per call)."""
+    if torch.cuda.current_device() == t.device.index:
+        return contextlib.nullcontext()
+    return torch.cuda.device(t.device)
 
 
 def _ptr(t):
@@ -172,7 +188,7 @@ def _act_fwd(op, x, y, codes, stream):
     dt = _dtype_code(x)
     y = _like(x, y, "y")
     codes = _codes_out(x.numel(), x.device, codes)
-    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+    with _device_of(x):   # launches go to the tensors' GPU
         _check(op, getattr(lib(), op)(dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes), _stream(x, stream)))
     return y, codes
 
@@ -184,7 +200,7 @@ def _act_bwd(op, dy, codes, dx, stream):
     if codes.dtype != torch.int32 or codes.numel() < codes_words(dy.numel()):
         raise ValueError("codes must be the int32 buffer written by the forward")
     dx = _like(dy, dx, "dx")
-    with torch.cuda.device(dy.device):   # launches go to the tensors' GPU
+    with _device_of(dy):   # launches go to the tensors' GPU
         _check(op, getattr(lib(), op)(dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx), _stream(dy, stream)))
     return dx
 
@@ -224,7 +240,7 @@ def reswiglu2_fwd(g, u, h=None, s=None, codes=None, stream=None):
     h = _like(g, h, "h")
     s = _like(g, s, "s")
     codes = _codes_out(g.numel(), g.device, codes)
-    with torch.cuda.device(g.device):   # launches go to the tensors' GPU
+    with _device_of(g):   # launches go to the tensors' GPU
         _check("reswiglu2_fwd", lib().reswiglu2_fwd(dt, g.numel(), _ptr(g), _ptr(u), _ptr(h), _ptr(s),
                                                     _ptr(codes), _stream(g, stream)))
     return h, s, codes
@@ -241,7 +257,7 @@ def reswiglu2_bwd(dh, u, s, codes, dg=None, du=None, stream=None):
         raise ValueError("codes must be the int32 buffer written by the forward")
     dg = _like(dh, dg, "dg")
     du = _like(dh, du, "du")
-    with torch.cuda.device(dh.device):   # launches go to the tensors' GPU
+    with _device_of(dh):   # launches go to the tensors' GPU
         _check("reswiglu2_bwd", lib().reswiglu2_bwd(dt, dh.numel(), _ptr(dh), _ptr(u), _ptr(s), _ptr(codes),
                                                     _ptr(dg), _ptr(du), _stream(dh, stream)))
     return dg, du
@@ -271,7 +287,7 @@ def stepact_fwd(x, act, thresholds, bits, y=None, codes=None, stream=None):
         codes = torch.empty(words, dtype=torch.int32, device=x.device)
     elif _on(codes, x, "codes").dtype != torch.int32 or codes.numel() < words:
         raise ValueError(f"codes must be an int32 GPU tensor of at least {words} words")
-    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+    with _device_of(x):   # launches go to the tensors' GPU
         _check("stepact_fwd", lib().stepact_fwd(a, bits, tab, dt, x.numel(), _ptr(x), _ptr(y), _ptr(codes),
                                                 _stream(x, stream)))
     return y, codes
@@ -289,7 +305,7 @@ def stepact_bwd(dy, codes, levels, bits, dx=None, stream=None):
         raise ValueError("codes must be the int32 buffer written by the forward")
     tab = _doubles(levels, 1 << bits, "levels")
     dx = _like(dy, dx, "dx")
-    with torch.cuda.device(dy.device):   # launches go to the tensors' GPU
+    with _device_of(dy):   # launches go to the tensors' GPU
         _check("stepact_bwd", lib().stepact_bwd(bits, tab, dt, dy.numel(), _ptr(dy), _ptr(codes), _ptr(dx),
                                                 _stream(dy, stream)))
     return dx
@@ -314,7 +330,7 @@ def _norm_fwd(op, x, eps, z, rstd, stream):
         _on(rstd, x, "rstd")
         if rstd.dtype != torch.float32 or rstd.numel() != rows:
             raise ValueError("rstd must be float32 with one value per row")
-    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+    with _device_of(x):   # launches go to the tensors' GPU
         _check(op, getattr(lib(), op)(dt, rows, cols, float(eps), _ptr(x), _ptr(z), _ptr(rstd),
                                       _stream(x, stream)))
     return z, rstd
@@ -331,7 +347,7 @@ def _norm_bwd(op, dz, z, rstd, dx, stream):
     if rstd.dtype != torch.float32 or rstd.numel() != rows:
         raise ValueError("rstd must be float32 with one value per row")
     dx = _like(dz, dx, "dx")
-    with torch.cuda.device(dz.device):   # launches go to the tensors' GPU
+    with _device_of(dz):   # launches go to the tensors' GPU
         _check(op, getattr(lib(), op)(dt, rows, cols, _ptr(dz), _ptr(z), _ptr(rstd), _ptr(dx),
                                       _stream(dz, stream)))
     return dx
@@ -364,7 +380,7 @@ def copy_bytes(src, dst, stream=None):
     nbytes = src.numel() * src.element_size()
     if dst.numel() * dst.element_size() != nbytes:
         raise ValueError("src and dst must have the same byte size")
-    with torch.cuda.device(src.device):   # launches go to the tensors' GPU
+    with _device_of(src):   # launches go to the tensors' GPU
         _check("lmbp_copy", lib().lmbp_copy(_ptr(src), _ptr(dst), nbytes, _stream(src, stream)))
     return dst
 
@@ -403,7 +419,7 @@ def linear_act_fwd(x, w, bias=None, act="gelu", y=None, codes=None, z=None, stor
             raise ValueError("z must be a bfloat16 tensor of m * n elements")
     codes = _codes_out(m * n, x.device, codes)
     L = lib()
-    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+    with _device_of(x):   # launches go to the tensors' GPU
         _check("linear_act_fwd", L.linear_act_fwd(ACT_GELU if act == "gelu" else ACT_SILU, BF16, m, n, k,
                                                   _ptr(x), _ptr(w),
                                                   _ptr(bias) if bias is not None else None,
@@ -439,7 +455,7 @@ def linear_swiglu_fwd(x, w_gate, w_up, h=None, s=None, u=None, codes=None, g=Non
     if g is not None or store_g:
         g = out(g, "g")
     codes = _codes_out(m * n, x.device, codes)
-    with torch.cuda.device(x.device):   # launches go to the tensors' GPU
+    with _device_of(x):   # launches go to the tensors' GPU
         _check("linear_swiglu_fwd", lib().linear_swiglu_fwd(
             BF16, m, n, k, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(h), _ptr(s), _ptr(u), _ptr(codes),
             _ptr(g) if g is not None else None, _stream(x, stream)))
