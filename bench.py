@@ -586,6 +586,9 @@ def main():
     ap.add_argument("--workload", default=WORKLOAD,
                     help="the step's tensors (a name from inputs.WORKLOADS; the default is the "
                          "LLaMA-7B-shaped configuration the metric is quoted on)")
+    ap.add_argument("--graph", action="store_true",
+                    help="replay the timed steps and per-kernel loops from HIP graphs instead of launching "
+                         "them from Python (for workloads whose kernels are shorter than a Python launch)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--swiglu", action="store_true",
                     help="use ReSiLU2 fused with the SwiGLU product (h = SiLU(g) * u) in the step")
@@ -664,7 +667,8 @@ def main():
                 self.s = torch.empty_like(g)
                 self.du = torch.empty_like(u)
 
-        def kernels(self):
+        def kernels(self, stream):
+            # stream None: the current stream (what a graph capture records).
             if self.u is None:
                 act = [lambda: afwd(self.g, y=self.h, codes=self.codes, stream=stream),
                        lambda: abwd(self.dy, self.codes, dx=self.dg, stream=stream)]
@@ -684,14 +688,29 @@ def main():
     clone = lambda t: None if t is None else t.clone()
     sets = [Set(x, dz, g, dy, u)] + [Set(x.clone(), dz.clone(), g.clone(), dy.clone(), clone(u))
                                      for _ in range(2)]
-    ks = [st.kernels() for st in sets]
+    ks = [st.kernels(stream) for st in sets]
+    kc = [st.kernels(None) for st in sets]   # for graph capture
 
-    def step(k):
-        f, b = ks[k % 3], ks[(k - 1) % 3]
+    def step(k, kl=ks):
+        f, b = kl[k % 3], kl[(k - 1) % 3]
         f[0]()
         f[1]()
         b[2]()
         b[3]()
+
+    def captured(fn):
+        """A HIP graph of what fn() launches on the current stream (captured on a side
+        stream after one eager pass there, as torch requires)."""
+        side = torch.cuda.Stream(dev)
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            fn()
+        stream.wait_stream(side)
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        torch.cuda.synchronize()
+        return graph
 
     for st in ks:          # every set holds valid saved state before the first step
         st[0]()
@@ -701,36 +720,51 @@ def main():
     torch.cuda.synchronize()
     print(f"[bench] warmup {args.warmup} steps done; timing {args.steps}", file=sys.stderr, flush=True)
 
-    # Timed region: K steps back to back, bracketed by events on the kernels' stream.
+    # Timed region: K steps back to back, bracketed by events on the kernels' stream,
+    # launched from Python; with --graph the K steps are replayed from one HIP graph (the
+    # same launches without the host in the loop, which small workloads need; on this stack
+    # a graph node costs slightly more GPU time than a back-to-back launch, so it is not the
+    # default).
     mk = lambda: torch.cuda.Event(enable_timing=True)
     start, end = mk(), mk()
+    k0 = args.warmup
+    graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     start.record(stream)
-    for k in range(args.steps):
-        step(args.warmup + k)
+    if graph is None:
+        for k in range(args.steps):
+            step(k0 + k)
+    else:
+        graph.replay()
     end.record(stream)
     torch.cuda.synchronize()
     t_wall = time.perf_counter() - t_wall0
     ms_total = start.elapsed_time(end)
     ms_step = ms_total / args.steps
+    del graph
 
-    # Per-kernel launch duration: each kernel launched back to back, cycling over the
-    # three tensor sets (consecutive launches do not share a working set), timed with
-    # events around the launches on the same stream.
+    # Per-kernel launch duration: each kernel launched K times back to back, cycling over
+    # the three tensor sets (consecutive launches do not share a working set), timed with
+    # events around the launches on the same stream (replayed from a graph with --graph).
     print("[bench] per-kernel timing", file=sys.stderr, flush=True)
     per_kernel_ms = {}
     for i, n in enumerate(names):
         for j in range(3):
             ks[j % 3][i]()
+        g_i = None if not args.graph else captured(lambda: [kc[j % 3][i]() for j in range(args.steps)])
         a, b = mk(), mk()
         a.record(stream)
-        for j in range(args.steps):
-            ks[j % 3][i]()
+        if g_i is None:
+            for j in range(args.steps):
+                ks[j % 3][i]()
+        else:
+            g_i.replay()
         b.record(stream)
         torch.cuda.synchronize()
         per_kernel_ms[n] = a.elapsed_time(b) / args.steps
-    del sets, ks
+        del g_i
+    del sets, ks, kc
 
     # Plain-copy reference of known size: the practical streaming ceiling, and the
     # calibration point for hardware byte counters.
@@ -806,6 +840,7 @@ def main():
         # (B_fwd + B_bwd) / (t_fwd + t_bwd) summed over both pairs); `value` is the wall-clock rate.
         "kernels_only_GBps": round(bytes_step / (sum(per_kernel_ms.values()) * 1e-3) / 1e9, 1),
         "wall_s_timed": round(t_wall, 4),
+        "launch": "hip_graph" if args.graph else "eager",
     }
     if args.pairs:
         print("[bench] op pairs on every workload", file=sys.stderr, flush=True)

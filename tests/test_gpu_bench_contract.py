@@ -13,7 +13,8 @@ pytestmark = pytest.mark.gpu
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-@pytest.mark.parametrize("flags", [[], ["--swiglu"]], ids=["plain", "swiglu"])
+@pytest.mark.parametrize("flags", [[], ["--swiglu"], ["--workload", "vit_b_fp32", "--graph"]],
+                         ids=["plain", "swiglu", "vit_fp32_graph"])
 def test_bench_prints_one_contract_line(flags):
     print(f"[bench contract] bench.py --steps 5 --warmup 5 --no-cpu-baseline {' '.join(flags)}", flush=True)
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--steps", "5", "--warmup", "5",
@@ -29,6 +30,9 @@ def test_bench_prints_one_contract_line(flags):
     assert d["n_gpus"] == 1 and d["steps"] == 5 and d["warmup"] == 5
     assert d["unit"] == "GB/s" and d["higher_is_better"] is True and d["data"] == "synthetic"
     assert "workload" in d["config"]
+    assert d["launch"] == ("hip_graph" if "--graph" in flags else "eager")
+    if "--workload" in flags:
+        assert d["config"]["workload"] == flags[flags.index("--workload") + 1]
     step_bytes = d["config"]["bytes_per_step"]
     assert d["value"] == pytest.approx(step_bytes / (d["ms_per_step"] * 1e-3) / 1e9, rel=2e-3)
     rf = d["roofline"]
