@@ -17,13 +17,20 @@ event-timed loop that launches each kernel back to back over rotating tensor
 sets; the dominant kernel's figure feeds the roofline entry.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--swiglu] [--pairs]
-                      [--linear]
+                      [--linear] [--blocks] [--variants] [--workload NAME] [--graph]
 
+--workload runs the same step on another configured workload (ViT-B fp32, ViT-B
+batch 64 bf16 x 12 blocks, LLaMA-13B with outliers). --graph replays the timed
+steps from one HIP graph instead of launching them from Python (for workloads
+whose kernels are shorter than a Python launch); the JSON line names the mode
+in "launch".
 --linear adds the fused linear-layer + activation forward (TFLOP/s, against the
 unfused library GEMM + activation kernel) on the ViT-B and LLaMA-7B MLP shapes.
 --pairs adds, for every workload (ViT-B fp32, ViT-B batch 64 bf16 x 12 blocks,
 LLaMA-7B and LLaMA-13B shapes), the forward + backward GB/s of the norm pair and
 of the activation pair, cold and warm.
+--blocks adds a bf16 training step of whole MLP blocks against torch's modules;
+--variants the k-bit family kernels (k = 1..4, ReGELU2-d).
 """
 
 import argparse
