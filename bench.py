@@ -34,6 +34,7 @@ of the activation pair, cold and warm.
 """
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -735,7 +736,15 @@ def main():
     mk = lambda: torch.cuda.Event(enable_timing=True)
     start, end = mk(), mk()
     k0 = args.warmup
+
+    # Python's garbage collector is off while the timed loops launch (a collection pass
+    # in the first steps, before the host has run ahead of the GPU, would leave the GPU
+    # idle inside the timed region). Holding the stream on a GPU-side spin so the host
+    # could run ahead instead was slower: the idle GPU lowered its clocks during the
+    # spin, and the first timed steps ran slower.
     graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
+    gc.collect()
+    gc.disable()
     torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     start.record(stream)
@@ -789,6 +798,7 @@ def main():
     torch.cuda.synchronize()
     copy_ms = a.elapsed_time(b) / args.steps
     del pairs
+    gc.enable()
 
     bytes_step = sum(nb.values())
     value = bytes_step / (ms_step * 1e-3) / 1e9
