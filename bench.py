@@ -588,7 +588,7 @@ def block_report(torch, dev, reps):
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=200,
                     help="untimed steps first; a few hundred bring the clocks to their steady state")
     ap.add_argument("--workload", default=WORKLOAD,
@@ -723,6 +723,15 @@ def main():
     for st in ks:          # every set holds valid saved state before the first step
         st[0]()
         st[1]()
+    k0 = args.warmup
+    graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
+    # Python's garbage collector runs once here and is then off from the warm-up through
+    # the timed loops. A collection takes tens of ms; a GPU left idle that long before the
+    # timed region lowers its clocks, and the first timed steps ran slower (as they did
+    # when the stream was held on a GPU-side spin so that the host could run ahead); a
+    # collection inside the timed loop would leave the GPU idle there.
+    gc.collect()
+    gc.disable()
     for k in range(args.warmup):
         step(k)
     torch.cuda.synchronize()
@@ -735,17 +744,6 @@ def main():
     # default).
     mk = lambda: torch.cuda.Event(enable_timing=True)
     start, end = mk(), mk()
-    k0 = args.warmup
-
-    # Python's garbage collector is off while the timed loops launch (a collection pass
-    # in the first steps, before the host has run ahead of the GPU, would leave the GPU
-    # idle inside the timed region). Holding the stream on a GPU-side spin so the host
-    # could run ahead instead was slower: the idle GPU lowered its clocks during the
-    # spin, and the first timed steps ran slower.
-    graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
-    gc.collect()
-    gc.disable()
-    torch.cuda.synchronize()
     t_wall0 = time.perf_counter()
     start.record(stream)
     if graph is None:
