@@ -258,10 +258,7 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void glu_fwd_kernel(const void* g, 
       IO::unpack(vg[j], fg);
       IO::unpack(vu[j], fu);
 #pragma unroll
-      for (int e = 0; e < E; ++e) {
-        fs[e] = act_value<ACT, kPrecise>(fg[e]);
-        fu[e] = fs[e] * fu[e];
-      }
+      for (int e = 0; e < E; ++e) gated_value<ACT, kPrecise>(fg[e], fu[e], fs[e], fu[e]);
       part[j] = codes_of<A>(fg);
       stb16<LMBP_GLU_STORE_CPOL>(vec_rsrc(s, vbase, VPL * kWave), j * kWave + lane, IO::pack(fs));
       stb16<LMBP_GLU_STORE_CPOL>(vec_rsrc(h, vbase, VPL * kWave), j * kWave + lane, IO::pack(fu));
@@ -279,9 +276,10 @@ __global__ __launch_bounds__(LMBP_ACT_BLOCK) void glu_fwd_kernel(const void* g, 
       if (i < n) {
         const float gv = IO::load1(g, i);
         const float uv = IO::load1(u, i);
-        const float sv = act_value<ACT, kPrecise>(gv);
+        float sv, hv;
+        gated_value<ACT, kPrecise>(gv, uv, sv, hv);
         IO::store1(s, i, sv);
-        IO::store1(h, i, sv * uv);
+        IO::store1(h, i, hv);
         word |= seg_code<A>(gv) << (2 * e);
       }
     }

@@ -333,11 +333,6 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
     float f0[8], f1[8], o0[8], o1[8];
     BF16::unpack(v0, f0);
     BF16::unpack(v1, f1);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      o0[e] = act_value<ACT, false>(f0[e]);
-      o1[e] = act_value<ACT, false>(f1[e]);
-    }
     const int64_t base = (m0 + row) * N + n0 + c16;   // flat element index, multiple of 16
     if constexpr (GLU) {
       // Same arithmetic as the SwiGLU activation kernel on stored g and u.
@@ -348,8 +343,8 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
       BF16::unpack(u1, g1);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        g0[e] = o0[e] * g0[e];
-        g1[e] = o1[e] * g1[e];
+        gated_value<ACT, false>(f0[e], g0[e], o0[e], g0[e]);
+        gated_value<ACT, false>(f1[e], g1[e], o1[e], g1[e]);
       }
       *reinterpret_cast<u32x4*>(a.y + base) = BF16::pack(g0);
       *reinterpret_cast<u32x4*>(a.y + base + 8) = BF16::pack(g1);
@@ -358,6 +353,11 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
       *reinterpret_cast<u32x4*>(a.u + base) = u0;
       *reinterpret_cast<u32x4*>(a.u + base + 8) = u1;
     } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        o0[e] = act_value<ACT, false>(f0[e]);
+        o1[e] = act_value<ACT, false>(f1[e]);
+      }
       *reinterpret_cast<u32x4*>(a.y + base) = BF16::pack(o0);
       *reinterpret_cast<u32x4*>(a.y + base + 8) = BF16::pack(o1);
     }

@@ -18,9 +18,12 @@ to eps, so dx is of order eps) the output RMS is no measure of the arithmetic.
 There s_row is max(rms(ref), rstd * rms(dz)) (``norm_grad_scale``).
 
 Strict rules (activations): the forward value is within rtol relative for every
-element with |ref| >= 2^-60 (below that the result is at the edge of the fp32
-range and only the mixed rule applies); the backward value is within rtol
-relative everywhere and is exactly +-0 where the code is 0.
+element with |ref| >= 2^-126, the smallest normal fp32 / bf16 magnitude (below it
+the result is subnormal in both storage formats and only the mixed rule applies);
+the backward value is within rtol relative everywhere and is exactly +-0 where the
+code is 0. Products of two storage values (the SwiGLU gradients dg = dh u slope and
+du = dh s) can fall below the smallest normal and below bf16's subnormal range, so for
+them the strict rule applies where |ref| >= 2^-126, like the forward's.
 
 Integer outputs (codes) are compared bit for bit.
 """
@@ -63,7 +66,10 @@ def assert_mixed(got, ref, rtol, what, row_scale=None):
     return float(np.max(err / np.maximum(lim, 1e-300)))
 
 
-def assert_rel(got, ref, rtol, what, floor=2.0 ** -60):
+NORMAL_MIN = 2.0 ** -126
+
+
+def assert_rel(got, ref, rtol, what, floor=NORMAL_MIN):
     g = np.asarray(got, dtype=np.float64).reshape(-1)
     r = np.asarray(ref, dtype=np.float64).reshape(-1)
     m = (np.abs(r) >= floor) & (r != 0)

@@ -399,3 +399,63 @@ def pin_swiglu_reduces_to_resilu2(fwd, bwd, act_fwd, act_bwd, seed=6):
     err = max(float(np.max(np.abs(h - y))), float(np.max(np.abs(s - y))),
               float(np.max(np.abs(dg - act_bwd(dh, w2)))), float(np.max(np.abs(du - dh * y))))
     return bad + err
+
+
+# ------------------------------------------------- general k-bit family
+
+def pin_stepact_fd(stepact_fwd, stepact_bwd, relu_family, a, c, bits, act, seed=11):
+    """Composed k-bit forward + backward against what the mathematics fixes, at points
+    at least 1e-3 from every bias:
+    * the forward value against torch's float64 GELU (erf form, on [-4, 4]) or SiLU;
+    * dx of the backward, fed the forward's packed words, against dy times the central
+      finite-difference slope of the ReLU combination h~_{a,c} (eq. relus_family for
+      general k; the slope of segment j is the sum of the first j weights).
+    Returns the larger of the two maximum errors (relative for the value, absolute for
+    dx with dy ~ N(0, 1))."""
+    x = _kink_free_points(c, 1500, seed, lo=min(c) - 3.0, hi=max(c) + 3.0)
+    # odd-length tail so that the last packed word is partial
+    x = x[: x.size - (x.size % (32 // bits)) - 1]
+    dy = np.random.default_rng(seed + 1).normal(size=x.size)
+    y, words = stepact_fwd(x, act, c, bits)
+    xt = torch.from_numpy(x)
+    ref = (F.gelu(xt, approximate="none") if act == "gelu" else F.silu(xt)).numpy()
+    # torch's erf-form GELU cancels for x < -4 (1 + erf), so the value is compared on
+    # [-4, 4] for GELU, everywhere for SiLU
+    mask = (ref != 0) & ((np.abs(x) <= 4.0) if act == "gelu" else True)
+    e_y = float(np.max(np.abs(y[mask] - ref[mask]) / np.abs(ref[mask])))
+    # levels as the slopes of the combination itself, not through the oracle's helper;
+    # h~ is linear within 1e-3 of every point used, so a step of 1e-4 is exact up to
+    # rounding
+    h = 1e-4
+    fd = (relu_family(x + h, a, c) - relu_family(x - h, a, c)) / (2 * h)
+    seg_slopes = np.zeros(len(c) + 1)
+    for j in range(len(c) + 1):
+        lo = c[j - 1] if j > 0 else c[0] - 10.0
+        hi = c[j] if j < len(c) else c[-1] + 10.0
+        mid = 0.5 * (lo + hi)
+        seg_slopes[j] = (relu_family(np.array([mid + h]), a, c)[0]
+                         - relu_family(np.array([mid - h]), a, c)[0]) / (2 * h)
+    dx = stepact_bwd(dy, words, seg_slopes, bits)
+    e_dx = float(np.max(np.abs(dx - dy * fd)))
+    return max(e_y, e_dx)
+
+
+def pin_stepact_words_brute(stepact_fwd, c, bits, act="gelu", seed=12):
+    """Packed words of the composed forward against codes counted per element in a
+    Python loop and packed bit by bit (floor(32/k) codes per word, least significant
+    first, zero tail). Returns the number of words that differ (or -1 on a size
+    mismatch)."""
+    per = 32 // bits
+    r = np.random.default_rng(seed)
+    x = np.concatenate([r.normal(0, 3, 3 * per + 5), np.asarray(c) + 1e-9, np.asarray(c) - 1e-9])
+    _, words = stepact_fwd(x, act, c, bits)
+    want = [0] * ((x.size + per - 1) // per)
+    for i, xi in enumerate(x):
+        k = 0
+        for ci in c:
+            if xi > ci:
+                k += 1
+        want[i // per] |= k << (bits * (i % per))
+    if len(words) != len(want):
+        return -1
+    return sum(int(int(w) != v) for w, v in zip(words, want))

@@ -6,6 +6,7 @@ import torch
 from torch import nn
 
 import oracle
+import paper_2406_16282_amd as lmbp
 from paper_2406_16282_amd import inputs
 from paper_2406_16282_amd.nn import (MSLayerNorm, MSRMSNorm, ReGELU2, ReSiLU2, ReSwiGLU2,
                                      merge_norm_into_linears)
@@ -50,12 +51,16 @@ def test_swiglu_module():
     h = ReSwiGLU2()(gt, ut)
     h.backward(T(dh))
     h_o, s_o, w_o = oracle.reswiglu2_fwd(oracle.decode(g, "bf16"), oracle.decode(u, "bf16"))
-    # the backward sees the stored s (bf16), as the module saves it
-    dg_o, du_o = oracle.reswiglu2_bwd(oracle.decode(dh, "bf16"), oracle.decode(u, "bf16"),
-                                      oracle.round_to_dtype(s_o, "bf16"), w_o)
-    assert_rel(oracle.decode(H(h), "bf16"), h_o, 2e-2, "swiglu h")
-    assert_rel(oracle.decode(H(gt.grad), "bf16"), dg_o, 2e-2, "swiglu dg", floor=0.0)
-    assert_rel(oracle.decode(H(ut.grad), "bf16"), du_o, 2e-2, "swiglu du", floor=0.0)
+    # The module's backward sees the s its own forward stored (bf16). That s is checked
+    # against the oracle's s (one rounding); du = dh * s is then checked against the product
+    # with that same stored s (one more rounding), so each rounding meets the bound once.
+    _, s_gpu, _ = lmbp.reswiglu2_fwd(T(g), T(u))
+    s_gpu = oracle.decode(H(s_gpu), "bf16")
+    dg_o, du_o = oracle.reswiglu2_bwd(oracle.decode(dh, "bf16"), oracle.decode(u, "bf16"), s_gpu, w_o)
+    assert_rel(s_gpu, s_o, 1e-2, "swiglu stored s")
+    assert_rel(oracle.decode(H(h), "bf16"), h_o, 1e-2, "swiglu h")
+    assert_rel(oracle.decode(H(gt.grad), "bf16"), dg_o, 1e-2, "swiglu dg")
+    assert_rel(oracle.decode(H(ut.grad), "bf16"), du_o, 1e-2, "swiglu du")
 
 
 @pytest.mark.parametrize("kind", ["ln", "rms"])
@@ -139,10 +144,10 @@ def test_fused_linear_act_module(which):
     obwd = oracle.regelu2_bwd if which == "gelu" else oracle.resilu2_bwd
     dz = oracle.decode(oracle.encode(obwd(oracle.decode(dy, "bf16"), c_o), "bf16"), "bf16")
     xd, wd = oracle.decode(x, "bf16"), oracle.decode(w, "bf16")
-    assert_mixed(oracle.decode(H(xt.grad), "bf16"), dz @ wd, 2e-2, "fused module dx")
-    assert_mixed(oracle.decode(H(mod.weight.grad), "bf16"), dz.T @ xd, 2e-2, "fused module dW")
+    assert_mixed(oracle.decode(H(xt.grad), "bf16"), dz @ wd, 1e-2, "fused module dx")
+    assert_mixed(oracle.decode(H(mod.weight.grad), "bf16"), dz.T @ xd, 1e-2, "fused module dW")
     assert_mixed(oracle.decode(H(mod.bias.grad), "bf16").reshape(1, -1), dz.sum(0).reshape(1, -1),
-                 2e-2, "fused module db")
+                 1e-2, "fused module db")
 
 
 
@@ -164,15 +169,15 @@ def test_fused_linear_swiglu_module():
     h = mod(xt)
     h.backward(T(dh))
     _, g_s, _, u_s, h_o, s_o, c_o = oracle.linear_swiglu_fwd(x, wg, wu)
-    assert_mixed(oracle.decode(H(h), "bf16"), h_o, 2e-2, "swiglu module h")
+    assert_mixed(oracle.decode(H(h), "bf16"), h_o, 1e-2, "swiglu module h")
     s_st = oracle.decode(oracle.encode(s_o, "bf16"), "bf16")
     dg_o, du_o = oracle.reswiglu2_bwd(oracle.decode(dh, "bf16"), oracle.decode(u_s, "bf16"), s_st, c_o)
     dg_o = oracle.decode(oracle.encode(dg_o, "bf16"), "bf16")
     du_o = oracle.decode(oracle.encode(du_o, "bf16"), "bf16")
     xd, wgd, wud = (oracle.decode(a, "bf16") for a in (x, wg, wu))
-    assert_mixed(oracle.decode(H(xt.grad), "bf16"), dg_o @ wgd + du_o @ wud, 2e-2, "swiglu module dx")
-    assert_mixed(oracle.decode(H(mod.gate.weight.grad), "bf16"), dg_o.T @ xd, 2e-2, "swiglu module dWg")
-    assert_mixed(oracle.decode(H(mod.up.weight.grad), "bf16"), du_o.T @ xd, 2e-2, "swiglu module dWu")
+    assert_mixed(oracle.decode(H(xt.grad), "bf16"), dg_o @ wgd + du_o @ wud, 1e-2, "swiglu module dx")
+    assert_mixed(oracle.decode(H(mod.gate.weight.grad), "bf16"), dg_o.T @ xd, 1e-2, "swiglu module dWg")
+    assert_mixed(oracle.decode(H(mod.up.weight.grad), "bf16"), du_o.T @ xd, 1e-2, "swiglu module dWu")
 
 
 def _saved_activation_bytes(run, params):

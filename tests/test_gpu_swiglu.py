@@ -7,7 +7,7 @@ import torch
 import oracle
 import paper_2406_16282_amd as lmbp
 from paper_2406_16282_amd import inputs
-from compare import assert_codes_equal, assert_mixed, assert_rel, rtol_for
+from compare import NORMAL_MIN, assert_codes_equal, assert_mixed, assert_rel, rtol_for
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -36,9 +36,11 @@ def check(dtype, g, u, dh, label):
     dec = lambda t: oracle.decode(H(t), dtype).reshape(shape2)
     assert_rel(dec(s), s_o.reshape(shape2), rtol, f"{label} s (strict)")
     assert_mixed(dec(h), h_o.reshape(shape2), rtol, f"{label} h")
-    assert_rel(dec(h), h_o.reshape(shape2), 2 * rtol, f"{label} h (strict)")
+    assert_rel(dec(h), h_o.reshape(shape2), rtol, f"{label} h (strict)")
     assert_mixed(dec(dg), dg_o.reshape(shape2), rtol, f"{label} dg")
-    assert_rel(dec(dg), dg_o.reshape(shape2), 2 * rtol, f"{label} dg (strict)", floor=0.0)
+    # products of two storage values can fall below the smallest normal (and below bf16's
+    # subnormal range): those are held to the mixed rule only, as forward outputs are
+    assert_rel(dec(dg), dg_o.reshape(shape2), rtol, f"{label} dg (strict)")
     assert_mixed(dec(du), du_o.reshape(shape2), rtol, f"{label} du")
     zero = oracle.unpack_codes(w_o, g.size).reshape(shape2) == 0
     assert np.all(dec(dg)[zero] == 0.0), "code-0 gradients must be exactly zero"
@@ -85,29 +87,49 @@ def test_in_place_and_misaligned():
         assert np.array_equal(H(a), H(b))
     h_o, s_o, w_o = oracle.reswiglu2_fwd(oracle.decode(g[1:], "bf16"), oracle.decode(u[1:], "bf16"))
     assert_codes_equal(H(c3), w_o, "misaligned codes")
-    assert_rel(oracle.decode(H(h3), "bf16"), h_o, 2e-2, "misaligned h")
+    assert_rel(oracle.decode(H(h3), "bf16"), h_o, 1e-2, "misaligned h")
 
 
 @pytest.mark.parametrize("name", ["llama7b_swiglu_bf16", "llama13b_outliers_bf16"])
 def test_full_size(name):
+    """Every element of h, s, codes, dg and du at the full LLaMA gate sizes, compared on
+    the host in blocks of rows. The backward is fed the oracle's saved state (s rounded
+    to the storage format, codes)."""
     w = inputs.WORKLOADS[name]
-    s = w.act
-    print(f"[swiglu full] {name}: [{s.rows}x{s.cols}]", flush=True)
-    g, u, dh = w.act_x(), w.act_u(), w.act_dy()
-    g64 = oracle.decode(g, s.dtype).reshape(-1)
-    w_o = oracle.pack_codes(oracle.segment_code(g64, oracle.SILU_C))
+    sp = w.act
+    print(f"[swiglu full] {name}: [{sp.rows}x{sp.cols}]", flush=True)
+    g = w.act_x().reshape(sp.rows, sp.cols)
+    u = w.act_u().reshape(sp.rows, sp.cols)
+    dh = w.act_dy().reshape(sp.rows, sp.cols)
     h, sv, codes = lmbp.reswiglu2_fwd(T(g), T(u))
-    dg, du = lmbp.reswiglu2_bwd(T(dh), T(u), sv, T(w_o))
     torch.cuda.synchronize()
-    assert_codes_equal(H(codes), w_o, f"{name} codes")
-    idx = np.sort(np.random.default_rng(0).choice(g64.size, size=200_000, replace=False))
-    u64 = oracle.decode(u, s.dtype).reshape(-1)[idx]
-    dh64 = oracle.decode(dh, s.dtype).reshape(-1)[idx]
-    sv_gpu = oracle.decode(H(sv).reshape(-1)[idx], s.dtype)
-    s_ref = oracle.silu(g64[idx])
-    assert_rel(sv_gpu, s_ref, 1e-2, f"{name} s (sample)")
-    assert_rel(oracle.decode(H(h).reshape(-1)[idx], s.dtype), s_ref * u64, 2e-2, f"{name} h (sample)")
-    lv = oracle.derivative_levels(oracle.SILU_A)[oracle.unpack_codes(w_o, g64.size)[idx]]
-    assert_rel(oracle.decode(H(dg).reshape(-1)[idx], s.dtype), dh64 * u64 * lv, 2e-2, f"{name} dg (sample)", floor=0.0)
-    # du = dh * s with the GPU's own saved s (the value the product rule sees)
-    assert_rel(oracle.decode(H(du).reshape(-1)[idx], s.dtype), dh64 * sv_gpu, 1e-2, f"{name} du (sample)", floor=0.0)
+    h_h, s_h, c_h = H(h).reshape(sp.rows, sp.cols), H(sv).reshape(sp.rows, sp.cols), H(codes)
+    del h, sv, codes
+    step = max(1, (8 << 20) // sp.cols)
+    per_row = sp.cols // 16
+    s_saved = np.empty_like(g)
+    w_all = []
+    rtol = rtol_for(sp.dtype)
+    for r0 in range(0, sp.rows, step):
+        r1 = min(sp.rows, r0 + step)
+        u64 = oracle.decode(u[r0:r1], sp.dtype)
+        h_o, s_o, w_o = oracle.reswiglu2_fwd(oracle.decode(g[r0:r1], sp.dtype), u64)
+        assert_codes_equal(c_h[r0 * per_row:r1 * per_row], w_o, f"{name} codes rows {r0}:{r1}")
+        assert_rel(oracle.decode(s_h[r0:r1], sp.dtype), s_o, rtol, f"{name} s rows {r0}:{r1}")
+        assert_rel(oracle.decode(h_h[r0:r1], sp.dtype), h_o, rtol, f"{name} h rows {r0}:{r1}")
+        s_saved[r0:r1] = oracle.encode(s_o, sp.dtype)
+        w_all.append(w_o)
+    del h_h, s_h
+    w_all = np.concatenate(w_all)
+    dg, du = lmbp.reswiglu2_bwd(T(dh), T(u), T(s_saved), T(w_all))
+    torch.cuda.synchronize()
+    dg_h, du_h = H(dg).reshape(sp.rows, sp.cols), H(du).reshape(sp.rows, sp.cols)
+    for r0 in range(0, sp.rows, step):
+        r1 = min(sp.rows, r0 + step)
+        dg_o, du_o = oracle.reswiglu2_bwd(oracle.decode(dh[r0:r1], sp.dtype), oracle.decode(u[r0:r1], sp.dtype),
+                                          oracle.decode(s_saved[r0:r1], sp.dtype),
+                                          w_all[r0 * per_row:r1 * per_row])
+        assert_rel(oracle.decode(dg_h[r0:r1], sp.dtype), dg_o, rtol, f"{name} dg rows {r0}:{r1}")
+        assert_rel(oracle.decode(du_h[r0:r1], sp.dtype), du_o, rtol, f"{name} du rows {r0}:{r1}")
+        assert np.all(oracle.decode(dg_h[r0:r1], sp.dtype)[dg_o == 0] == 0), "code-0 gradients must be zero"
+    print(f"[swiglu full] {name}: all {sp.rows * sp.cols} elements compared", flush=True)

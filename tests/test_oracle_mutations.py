@@ -173,3 +173,59 @@ def test_swiglu_dg_without_u_caught():
         return dg, dh * s
     assert pins.pin_swiglu_fd(oracle.reswiglu2_fwd, bad_bwd, oracle.relu_combination,
                               oracle.SILU_A, oracle.SILU_C) > 1e-2
+
+
+# ------------------------------------------------- general k-bit family
+
+def _kbit_table(bits):
+    r = np.random.default_rng(200 + bits)
+    m = (1 << bits) - 1
+    return list(r.normal(0, 0.5, m - 1)), list(np.linspace(-3.0, 3.0, m))
+
+
+def test_stepact_unpack_with_wrong_width_caught():
+    from oracle import variants as V
+    for bits, wrong in ((3, 2), (2, 4), (4, 3), (1, 2)):
+        def bad_bwd(dy, words, levels, b, _w=wrong):
+            dy = np.asarray(dy, dtype=np.float64)
+            codes = V.unpack_bits(words, _w, dy.size) % len(levels)
+            return dy * np.asarray(levels)[codes]
+        a, c = _kbit_table(bits)
+        try:
+            err = pins.pin_stepact_fd(V.stepact_fwd, bad_bwd, V.relu_family, a, c, bits, "gelu")
+        except ValueError:
+            continue   # a wider field yields too few codes: the shape mismatch is loud
+        assert err > 1e-2
+
+
+def test_stepact_level_index_off_by_one_caught():
+    from oracle import variants as V
+    for bits in (1, 2, 3, 4):
+        def bad_bwd(dy, words, levels, b):
+            dy = np.asarray(dy, dtype=np.float64)
+            codes = V.unpack_bits(words, b, dy.size)
+            return dy * np.asarray(levels)[np.minimum(codes + 1, len(levels) - 1)]
+        a, c = _kbit_table(bits)
+        assert pins.pin_stepact_fd(V.stepact_fwd, bad_bwd, V.relu_family, a, c, bits, "silu") > 1e-2
+
+
+def test_stepact_wrong_activation_or_packing_caught():
+    from oracle import variants as V
+    def swapped_act(x, act, c, bits):
+        return V.stepact_fwd(x, "silu" if act == "gelu" else "gelu", c, bits)
+    a, c = _kbit_table(3)
+    assert pins.pin_stepact_fd(swapped_act, V.stepact_bwd, V.relu_family, a, c, 3, "gelu") > 1e-3
+    def packed_as_k2(x, act, c, bits):
+        y, _ = V.stepact_fwd(x, act, c, bits)
+        return y, V.pack_bits(np.minimum(V.family_code(x, c), 3), 2)
+    assert pins.pin_stepact_words_brute(packed_as_k2, c, 3) != 0
+    def msb_first(x, act, c, bits):
+        y, _ = V.stepact_fwd(x, act, c, bits)
+        codes = V.family_code(x, c)
+        per = 32 // bits
+        w = np.zeros(V.words_for(bits, codes.size), dtype=np.uint32)
+        for slot in range(per):
+            part = codes[slot::per].astype(np.uint32)
+            w[: part.size] |= part << np.uint32(bits * (per - 1 - slot))
+        return y, w
+    assert pins.pin_stepact_words_brute(msb_first, c, 3) != 0

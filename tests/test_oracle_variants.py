@@ -77,3 +77,48 @@ def test_three_bit_family_codes_brute_force():
     assert np.array_equal(V.family_code(x, c), want)
     words = V.pack_bits(want, 3)
     assert np.array_equal(V.unpack_bits(words, 3, x.size), want)
+
+
+def _random_table(bits, seed):
+    r = np.random.default_rng(100 + seed)
+    m = (1 << bits) - 1
+    c = np.sort(r.uniform(-4, 4, m))
+    while m > 1 and np.min(np.diff(c)) < 1e-2:
+        c = np.sort(r.uniform(-4, 4, m))
+    return list(r.normal(0, 0.5, m - 1)), list(c)
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+def test_stepact_composed_against_torch_and_fd_slopes(bits, act):
+    a, c = _random_table(bits, bits)
+    assert pins.pin_stepact_fd(V.stepact_fwd, V.stepact_bwd, V.relu_family, a, c, bits, act) < 1e-8
+
+
+@pytest.mark.parametrize("table", ["gelu", "silu", "regelu2d"])
+def test_stepact_composed_with_paper_tables(table):
+    a, c, act = {"gelu": (oracle.GELU_A, oracle.GELU_C, "gelu"),
+                 "silu": (oracle.SILU_A, oracle.SILU_C, "silu"),
+                 "regelu2d": (V.REGELU2D_A, V.REGELU2D_C, "gelu")}[table]
+    assert pins.pin_stepact_fd(V.stepact_fwd, V.stepact_bwd, V.relu_family, list(a), list(c), 2,
+                               act) < 1e-8
+
+
+@pytest.mark.parametrize("bits", [1, 2, 3, 4])
+def test_stepact_words_against_a_bitwise_loop(bits):
+    _, c = _random_table(bits, 20 + bits)
+    assert pins.pin_stepact_words_brute(V.stepact_fwd, c, bits) == 0
+
+
+def test_stepact_k2_is_byte_equal_to_the_dedicated_k2_oracle():
+    """With Appendix E's tables and k = 2, the table-driven composition must give the
+    same values, the same words and the same gradients as ReGELU2 / ReSiLU2."""
+    r = np.random.default_rng(5)
+    x = np.concatenate([r.normal(0, 3, 4001), np.array(oracle.GELU_C), np.array(oracle.SILU_C)])
+    dy = r.normal(size=x.size)
+    for act, a, c, fwd, bwd in (("gelu", oracle.GELU_A, oracle.GELU_C, oracle.regelu2_fwd, oracle.regelu2_bwd),
+                                ("silu", oracle.SILU_A, oracle.SILU_C, oracle.resilu2_fwd, oracle.resilu2_bwd)):
+        y, w = V.stepact_fwd(x, act, c, 2)
+        y2, w2 = fwd(x)
+        assert np.array_equal(y, y2) and np.array_equal(w, w2)
+        assert np.array_equal(V.stepact_bwd(dy, w, V.family_levels(a), 2), bwd(dy, w2))
