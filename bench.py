@@ -14,7 +14,10 @@ is the algorithmic HBM traffic of the step (bytes each kernel must read and
 write) divided by the measured step time (K steps back to back between two HIP
 events on the kernels' stream). Per-kernel launch durations come from a second
 event-timed loop that launches each kernel back to back over rotating tensor
-sets; the dominant kernel's figure feeds the roofline entry.
+sets; the dominant kernel's figure feeds the roofline entry. The line also carries
+the cold forward + backward GB/s of the MS-LN and ReGELU2 pairs on the ViT-B
+batch-64 bf16 shapes (`pairs_vit_b_bs64_bf16`), and the CPU oracle's rate on the
+same step (timed after the GPU legs).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline] [--swiglu] [--pairs]
                       [--linear] [--blocks] [--variants] [--workload NAME] [--graph]
@@ -172,12 +175,11 @@ def cpu_baseline(w, tensors, min_seconds=10.0):
     }
 
 
-def cpu_baseline_all_cores(w, tensors, procs, min_seconds=5.0):
+def cpu_baseline_all_cores(w, tensors, pool, procs, min_seconds=5.0):
     """The same oracle on every host core at once: the step's rows split into `procs`
-    chunks, one worker process each (started fresh, before this process touches the
-    GPU), each repeating its chunk for `min_seconds`; rate = bytes of all chunk passes
-    over the longest worker's wall time."""
-    import multiprocessing as mp
+    chunks, one worker process each (the pool's processes are started before this
+    process touches the GPU and never touch it), each repeating its chunk for
+    `min_seconds`; rate = bytes of all chunk passes over the longest worker's wall time."""
     step_bytes = sum(algorithmic_bytes(w).values())
     x, dz, g, dy = tensors
     rn, ra = w.norm.rows, w.act.rows
@@ -186,8 +188,7 @@ def cpu_baseline_all_cores(w, tensors, procs, min_seconds=5.0):
         a, b = rn * i // procs, rn * (i + 1) // procs
         c, d = ra * i // procs, ra * (i + 1) // procs
         jobs.append((_spec(w), x[a:b], dz[a:b], g[c:d], dy[c:d], min_seconds))
-    with mp.get_context("spawn").Pool(procs) as pool:
-        res = pool.map(_oracle_chunk, jobs)
+    res = pool.map(_oracle_chunk, jobs)
     # The chunks split the rows evenly (within one row), each 1/procs of the step.
     passes = sum(p for p, _ in res) / procs
     wall = max(e for _, e in res)
@@ -201,7 +202,7 @@ def cpu_baseline_all_cores(w, tensors, procs, min_seconds=5.0):
     }
 
 
-def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
+def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30, workloads=None):
     """Forward + backward GB/s of each op pair (norm, activation) on every workload:
     (B_fwd + B_bwd) / (t_fwd + t_bwd) with algorithmic bytes, per-launch durations
     from HIP-graph replays (launch-bound small kernels would otherwise measure the
@@ -215,6 +216,8 @@ def pair_report(torch, lmbp, inputs, dev, reps=40, cold_bytes=1 << 30):
     out = {}
     mk = lambda: torch.cuda.Event(enable_timing=True)
     for name, w in inputs.WORKLOADS.items():
+        if workloads is not None and name not in workloads:
+            continue
         nb = algorithmic_bytes(w)
         names = list(nb)
         eps = float(np.float32(w.norm.eps))
@@ -628,18 +631,16 @@ def main():
     if args.swiglu and inputs.WORKLOADS[wl].act.op != "resilu2":
         sys.exit("--swiglu needs a SiLU workload")
 
-    # The CPU oracle runs first: its worker processes start from a process that has not
-    # touched the GPU yet.
-    cpu = {}
-    if not args.no_cpu_baseline and not args.swiglu:
-        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
-        w0 = inputs.WORKLOADS[wl]
-        tensors = (w0.norm_x(), w0.norm_dz(), w0.act_x(), w0.act_dy())
-        cpu["cpu_baseline"] = cpu_baseline(w0, tensors)
+    # The CPU oracle is timed after the GPU legs, so that the GPU is not left idle for the
+    # oracle's tens of seconds right before its timed region. Its all-cores worker pool is
+    # started here, before this process touches the GPU (a process that has initialised
+    # the GPU does not start programs).
+    run_cpu = not args.no_cpu_baseline and not args.swiglu
+    pool = procs = None
+    if run_cpu:
+        import multiprocessing as mp
         procs = max(1, min(16, os.cpu_count() or 1))
-        print(f"[bench] timing the CPU oracle on {procs} processes", file=sys.stderr, flush=True)
-        cpu["cpu_baseline_all_cores"] = cpu_baseline_all_cores(w0, tensors, procs)
-        del tensors
+        pool = mp.get_context("spawn").Pool(procs)
 
     import torch
     import paper_2406_16282_amd as lmbp
@@ -720,18 +721,16 @@ def main():
         torch.cuda.synchronize()
         return graph
 
+    # Python's garbage collector runs once here and is then off from the warm-up through
+    # the timed loops: a collection takes tens of ms, during which the GPU would sit idle
+    # right before (or, inside the loops, within) the timed region.
+    gc.collect()
+    gc.disable()
+    k0 = args.warmup
+    graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
     for st in ks:          # every set holds valid saved state before the first step
         st[0]()
         st[1]()
-    k0 = args.warmup
-    graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
-    # Python's garbage collector runs once here and is then off from the warm-up through
-    # the timed loops. A collection takes tens of ms; a GPU left idle that long before the
-    # timed region lowers its clocks, and the first timed steps ran slower (as they did
-    # when the stream was held on a GPU-side spin so that the host could run ahead); a
-    # collection inside the timed loop would leave the GPU idle there.
-    gc.collect()
-    gc.disable()
     for k in range(args.warmup):
         step(k)
     torch.cuda.synchronize()
@@ -764,7 +763,9 @@ def main():
     print("[bench] per-kernel timing", file=sys.stderr, flush=True)
     per_kernel_ms = {}
     for i, n in enumerate(names):
-        for j in range(3):
+        # two untimed rounds over the sets first, so that the host is well ahead of the
+        # GPU when the timed launches start (otherwise the first of them can wait for it)
+        for j in range(6):
             ks[j % 3][i]()
         g_i = None if not args.graph else captured(lambda: [kc[j % 3][i]() for j in range(args.steps)])
         a, b = mk(), mk()
@@ -857,6 +858,15 @@ def main():
         "wall_s_timed": round(t_wall, 4),
         "launch": "hip_graph" if args.graph else "eager",
     }
+    # The other ops the metric names, MS-LN and ReGELU2, on the ViT-B batch-64 bf16 shapes:
+    # cold forward + backward GB/s of each pair, launches replayed from HIP graphs (as
+    # --pairs reports them for every workload).
+    if not args.pairs:
+        print("[bench] MS-LN and ReGELU2 pairs on vit_b_bs64_bf16_x12", file=sys.stderr, flush=True)
+        vit = pair_report(torch, lmbp, inputs, dev, workloads=("vit_b_bs64_bf16_x12",))["vit_b_bs64_bf16_x12"]
+        out["pairs_vit_b_bs64_bf16"] = {rec["op"]: {k: rec[k] for k in ("fwd_us", "bwd_us", "bytes", "GBps",
+                                                                      "pct_of_peak")}
+                                        for rec in (vit["norm"], vit["act"])}
     if args.pairs:
         print("[bench] op pairs on every workload", file=sys.stderr, flush=True)
         out["pairs"] = pair_report(torch, lmbp, inputs, dev)
@@ -870,7 +880,14 @@ def main():
     if args.blocks:
         print("[bench] MLP blocks", file=sys.stderr, flush=True)
         out["blocks"] = block_report(torch, dev, reps=max(5, min(args.steps, 20)))
-    out.update(cpu)
+    if run_cpu:
+        print("[bench] timing the CPU oracle on a bounded sample", file=sys.stderr, flush=True)
+        tensors = (w.norm_x(), w.norm_dz(), w.act_x(), w.act_dy())
+        out["cpu_baseline"] = cpu_baseline(w, tensors)
+        print(f"[bench] timing the CPU oracle on {procs} processes", file=sys.stderr, flush=True)
+        out["cpu_baseline_all_cores"] = cpu_baseline_all_cores(w, tensors, pool, procs)
+        pool.close()
+        pool.join()
     print(json.dumps(out))
 
 

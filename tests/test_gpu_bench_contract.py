@@ -40,3 +40,9 @@ def test_bench_prints_one_contract_line(flags):
     assert rf["frac"] == pytest.approx(rf["achieved"] / rf["peak"], abs=1e-4)
     assert 0.3 < rf["frac"] < 1.0
     assert rf["kernel"] in d["per_kernel"]
+    # the metric's other ops, MS-LN and ReGELU2, on the ViT-B batch-64 bf16 shapes
+    vit = d["pairs_vit_b_bs64_bf16"]
+    assert set(vit) == {"msln", "regelu2"}
+    for rec in vit.values():
+        assert rec["GBps"] == pytest.approx(rec["bytes"] / ((rec["fwd_us"] + rec["bwd_us"]) * 1e-6) / 1e9, rel=2e-3)
+        assert 0.2 < rec["pct_of_peak"] / 100 < 1.0
