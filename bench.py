@@ -516,6 +516,31 @@ def linear_report(torch, lmbp, inputs, dev, reps):
     }
     print(f"[bench] linear {name}: fused {t_fused:.1f} us ({tf:.0f} TFLOP/s), unfused "
           f"{t_unfused:.1f} us (two library GEMMs + SwiGLU activation)", file=sys.stderr, flush=True)
+
+    # MS-RMSNorm in front of the same gated layer: the norm's statistics pass plus the GEMM
+    # that also writes the norm's output z, against the norm kernel followed by the fused
+    # gated layer on z (the same layer, the same saved z and rstd).
+    name = "llama7b_msrms_mlp_swiglu_bf16"
+    eps = float(np.float32(1e-5))
+    xn = T(inputs.normal((m, k), 1.0, "bf16", tensor_id=inputs.NORM_X))
+    zn = torch.empty_like(xn)
+    rstd = torch.empty(m, dtype=torch.float32, device=dev)
+    t_fused, t_unfused, t_norm = timed_all([
+        lambda: lmbp.msrms_linear_swiglu_fwd(xn, wg, wu, eps, h=h, s=s, u=u, codes=codes, z=zn, rstd=rstd),
+        lambda: (lmbp.msrms_fwd(xn, eps, z=zn, rstd=rstd),
+                 lmbp.linear_swiglu_fwd(zn, wg, wu, h=h, s=s, u=u, codes=codes)),
+        lambda: lmbp.msrms_fwd(xn, eps, z=zn, rstd=rstd)])
+    tf = flops / (t_fused * 1e-6) / 1e12
+    out[name] = {
+        "m": m, "n": n, "k": k, "act": "silu (SwiGLU), MS-RMSNorm in front", "bias": False,
+        "fused_us": round(t_fused, 1), "fused_TFLOPs": round(tf, 1),
+        "unfused_us": round(t_unfused, 1), "norm_kernel_us": round(t_norm, 1),
+        "speedup_vs_unfused": round(t_unfused / t_fused, 3),
+        "roofline": {"bound": "mfma", "achieved": round(tf, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4)},
+    }
+    print(f"[bench] linear {name}: fused {t_fused:.1f} us, unfused {t_unfused:.1f} us "
+          f"(norm kernel {t_norm:.1f} + fused gated layer)", file=sys.stderr, flush=True)
     return out
 
 

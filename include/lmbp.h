@@ -13,6 +13,9 @@
  *   linear_act_fwd                 a linear layer whose output goes through ReGELU2 /
  *                                  ReSiLU2, fused (the pre-activation stays on chip)
  *   linear_swiglu_fwd              the LLaMA MLP's two projections + SwiGLU, fused
+ *   msrms_linear_act_fwd           MS-RMSNorm, the merged linear layer and ReGELU2 /
+ *                                  ReSiLU2 forward, fused (the norm in the GEMM)
+ *   msrms_linear_swiglu_fwd        MS-RMSNorm and the LLaMA MLP's input side, fused
  *
  * Conventions shared by every call
  * --------------------------------
@@ -218,6 +221,50 @@ lmbp_status linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, in
 lmbp_status linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, const void *x,
                               const void *w_gate, const void *w_up, void *h, void *s, void *u,
                               uint32_t *codes, void *g, void *stream);
+
+/* ------------------------------------------------------------------------
+ * MS-RMSNorm in front of the fused linear layer (Sec. 5.2 eq. norm_linear, App. G
+ * Alg. 3): the norm's affine merged into W (and b), the normalised row z consumed by
+ * the linear layer and kept as the saved tensor of both.
+ *
+ *   rstd = 1 / sqrt(p^-1 |x|^2 + eps) per row of x (p = k), fp32;
+ *   z    = bf16( x rstd )              the norm's output: the same bytes (and rstd the
+ *                                      same bits) as msrms_fwd computes from x;
+ *   y, codes as linear_act_fwd / linear_swiglu_fwd, with the pre-activation
+ *        bf16( rstd (x W^T) + b )      i.e. the row scale is applied to the fp32 sums of
+ *                                      the products of x, before the bias: the linear
+ *                                      layer sees the normalised row before its storage
+ *                                      rounding (equal to z W^T + b in exact arithmetic;
+ *                                      not byte-equal to linear_act_fwd applied to z).
+ *
+ * One statistics pass over x writes rstd; then the GEMM runs on x, and after their K
+ * loops its blocks also write z (each row tile's columns shared out among the blocks of
+ * that row, x read again from the caches), so the norm's output traffic overlaps the
+ * matrix products of other blocks.
+ *
+ *   dt   : LMBP_BF16 only.
+ *   m,n,k, x, w, bias, y, codes : as linear_act_fwd, with k >= 8 when m > 0.
+ *   eps  : finite and > 0 (as msrms_fwd).
+ *   pre  : NULL (not stored) or m x n bf16: the rounded pre-activation, from which y
+ *          and codes are exactly what regelu2_fwd / resilu2_fwd compute (as
+ *          linear_act_fwd's z).
+ *   z    : m x k bf16, 16-byte aligned (required: the saved tensor).
+ *   rstd : m fp32, 4-byte aligned.
+ * No output may overlap another output or an input. The backward pass is the linear
+ * layer's (or SwiGLU's) backward on the kept tensors, then msrms_bwd(dz, z, rstd).
+ * ------------------------------------------------------------------------ */
+lmbp_status msrms_linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
+                                 float eps, const void *x, const void *w, const void *bias,
+                                 void *y, uint32_t *codes, void *pre, void *z, float *rstd,
+                                 void *stream);
+
+/* The gated form: MS-RMSNorm, then linear_swiglu_fwd's two projections and SwiGLU
+ * (g and u each bf16(rstd (x W^T))), z and rstd as above; h, s, u, codes and the
+ * optional g (NULL: not stored) as linear_swiglu_fwd. */
+lmbp_status msrms_linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, float eps,
+                                    const void *x, const void *w_gate, const void *w_up, void *h,
+                                    void *s, void *u, uint32_t *codes, void *g, void *z,
+                                    float *rstd, void *stream);
 
 /* ------------------------------------------------------------------------
  * Measurement utility (not part of the method): copies `bytes` bytes from src

@@ -19,7 +19,8 @@ What it computes, each function citing the passage it follows:
   ``dx = sigma^-1 (H - p^-1 z z^T) dz`` from the saved output alone.
 * ``linear``: a linear layer z = x W^T + b whose output, rounded once to bf16, feeds
   ReGELU2 / ReSiLU2 (the fused forward of the MLP's first projection), and the gated
-  form (two projections feeding ReSiLU2 inside SwiGLU).
+  form (two projections feeding ReSiLU2 inside SwiGLU); both also with MS-RMSNorm in
+  front (the norm's output feeding the merged layer, Sec. 5.2 eq. norm_linear).
 * ``dtypes``: decoding of fp32 / bf16 storage to fp64 and correct round-to-nearest-even
   encoding of fp64 results back to storage.
 
@@ -38,7 +39,8 @@ from .activations import (
 )
 from .norms import msln_fwd, msln_bwd, msrms_fwd, msrms_bwd
 from . import variants
-from .linear import linear, linear_act_fwd, linear_swiglu_fwd
+from .linear import (linear, linear_act_fwd, linear_swiglu_fwd, msrms_linear_act_fwd,
+                     msrms_linear_swiglu_fwd)
 
 __all__ = [
     "decode", "encode", "round_to_dtype", "DTYPES",
@@ -48,5 +50,5 @@ __all__ = [
     "regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd",
     "reswiglu2_fwd", "reswiglu2_bwd",
     "msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd", "variants",
-    "linear", "linear_act_fwd", "linear_swiglu_fwd",
+    "linear", "linear_act_fwd", "linear_swiglu_fwd", "msrms_linear_act_fwd", "msrms_linear_swiglu_fwd",
 ]

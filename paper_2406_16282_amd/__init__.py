@@ -6,7 +6,8 @@ ReGELU2 / ReSiLU2 keep the exact activation in the forward pass and save only a
 pass (Sec. 4.2); ReSiLU2 also comes fused with the SwiGLU product of the LLaMA
 MLP, and both come fused into the epilogue of the preceding linear layer's matrix
 product (bf16 MFMA). MS-LN / MS-RMSNorm, with the affine merged into the next
-linear layer, save only their output and one fp32 statistic per row (Sec. 5.2).
+linear layer, save only their output and one fp32 statistic per row (Sec. 5.2);
+MS-RMSNorm also comes fused into that linear layer's matrix product.
 
 The kernels live in liblmbp.so (C ABI in include/lmbp.h); ``binding`` marshals
 torch tensors into it. The library is loaded on first use.
@@ -24,6 +25,8 @@ from .binding import (  # noqa: F401
     msln_fwd,
     msrms_bwd,
     msrms_fwd,
+    msrms_linear_act_fwd,
+    msrms_linear_swiglu_fwd,
     regelu2_bwd,
     regelu2_fwd,
     resilu2_bwd,

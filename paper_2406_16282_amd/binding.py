@@ -24,7 +24,7 @@ ACT_OPS = ("regelu2_fwd", "regelu2_bwd", "resilu2_fwd", "resilu2_bwd")
 NORM_OPS = ("msln_fwd", "msln_bwd", "msrms_fwd", "msrms_bwd")
 GLU_OPS = ("reswiglu2_fwd", "reswiglu2_bwd")
 STEP_OPS = ("stepact_fwd", "stepact_bwd")
-LINEAR_OPS = ("linear_act_fwd", "linear_swiglu_fwd")
+LINEAR_OPS = ("linear_act_fwd", "linear_swiglu_fwd", "msrms_linear_act_fwd", "msrms_linear_swiglu_fwd")
 ACT_GELU, ACT_SILU = 0, 1
 
 
@@ -81,6 +81,10 @@ def lib():
     L.linear_act_fwd.restype = i32
     L.linear_swiglu_fwd.argtypes = [i32, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp]
     L.linear_swiglu_fwd.restype = i32
+    L.msrms_linear_act_fwd.argtypes = [i32, i32, i64, i64, i64, f32, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.msrms_linear_act_fwd.restype = i32
+    L.msrms_linear_swiglu_fwd.argtypes = [i32, i64, i64, i64, f32, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]
+    L.msrms_linear_swiglu_fwd.restype = i32
     L.lmbp_copy.argtypes = [vp, vp, i64, vp]
     L.lmbp_copy.restype = i32
     _lib = L
@@ -460,3 +464,98 @@ def linear_swiglu_fwd(x, w_gate, w_up, h=None, s=None, u=None, codes=None, g=Non
             BF16, m, n, k, _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(h), _ptr(s), _ptr(u), _ptr(codes),
             _ptr(g) if g is not None else None, _stream(x, stream)))
     return (h, s, u, codes, g) if g is not None else (h, s, u, codes)
+
+
+def _norm_outs(x, m, k, z, rstd):
+    if z is None:
+        z = torch.empty(x.shape, dtype=torch.bfloat16, device=x.device)
+    else:
+        _on(z, x, "z")
+        if z.dtype != torch.bfloat16 or z.numel() != m * k:
+            raise ValueError("z must be a bfloat16 tensor of m * k elements")
+    if rstd is None:
+        rstd = torch.empty(m, dtype=torch.float32, device=x.device)
+    else:
+        _on(rstd, x, "rstd")
+        if rstd.dtype != torch.float32 or rstd.numel() != m:
+            raise ValueError("rstd must be a float32 tensor of m elements")
+    return z, rstd
+
+
+def msrms_linear_act_fwd(x, w, eps, bias=None, act="silu", y=None, codes=None, z=None, rstd=None,
+                         pre=None, store_pre=False, stream=None):
+    """MS-RMSNorm + fused linear layer + ReGELU2 / ReSiLU2 forward (bf16): rstd and
+    z = bf16(x rstd) as msrms_fwd, y = act(bf16(rstd (x W^T) + b)) and its codes.
+    Returns (y, codes, z, rstd) or, with store_pre (or a pre tensor given),
+    (y, codes, z, rstd, pre) with pre the rounded pre-activation."""
+    if act not in ("gelu", "silu"):
+        raise ValueError("act must be 'gelu' or 'silu'")
+    _dev(x, "x")
+    _on(w, x, "w")
+    if x.dtype != torch.bfloat16 or w.dtype != torch.bfloat16:
+        raise TypeError("msrms_linear_act_fwd takes bfloat16 x and w")
+    if w.dim() != 2 or x.shape[-1] != w.shape[1]:
+        raise ValueError("x must be [..., k] and w [n, k]")
+    n, k = w.shape
+    m = math.prod(x.shape[:-1])
+    out_shape = (*x.shape[:-1], n)
+    if bias is not None:
+        _on(bias, x, "bias")
+        if bias.dtype != torch.bfloat16 or bias.numel() != n:
+            raise ValueError("bias must be a bfloat16 tensor of n elements")
+    if y is None:
+        y = torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
+    else:
+        _on(y, x, "y")
+        if y.dtype != torch.bfloat16 or y.numel() != m * n:
+            raise ValueError("y must be a bfloat16 tensor of m * n elements")
+    z, rstd = _norm_outs(x, m, k, z, rstd)
+    if pre is None and store_pre:
+        pre = torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
+    elif pre is not None:
+        _on(pre, x, "pre")
+        if pre.dtype != torch.bfloat16 or pre.numel() != m * n:
+            raise ValueError("pre must be a bfloat16 tensor of m * n elements")
+    codes = _codes_out(m * n, x.device, codes)
+    with _device_of(x):   # launches go to the tensors' GPU
+        _check("msrms_linear_act_fwd", lib().msrms_linear_act_fwd(
+            ACT_GELU if act == "gelu" else ACT_SILU, BF16, m, n, k, float(eps), _ptr(x), _ptr(w),
+            _ptr(bias) if bias is not None else None, _ptr(y), _ptr(codes),
+            _ptr(pre) if pre is not None else None, _ptr(z), _ptr(rstd), _stream(x, stream)))
+    return (y, codes, z, rstd, pre) if pre is not None else (y, codes, z, rstd)
+
+
+def msrms_linear_swiglu_fwd(x, w_gate, w_up, eps, h=None, s=None, u=None, codes=None, z=None, rstd=None,
+                            g=None, store_g=False, stream=None):
+    """MS-RMSNorm + the fused LLaMA MLP input side (bf16): rstd and z = bf16(x rstd) as
+    msrms_fwd; g, u = bf16(rstd (x W^T)); h = SiLU(g) u, s = SiLU(g), codes of g.
+    Returns (h, s, u, codes, z, rstd) or, with store_g (or a g tensor given),
+    (h, s, u, codes, z, rstd, g)."""
+    for t, nm in ((x, "x"), (w_gate, "w_gate"), (w_up, "w_up")):
+        _on(t, x, nm)
+        if t.dtype != torch.bfloat16:
+            raise TypeError("msrms_linear_swiglu_fwd takes bfloat16 tensors")
+    if w_gate.dim() != 2 or w_gate.shape != w_up.shape or x.shape[-1] != w_gate.shape[1]:
+        raise ValueError("x must be [..., k], w_gate and w_up [n, k]")
+    n, k = w_gate.shape
+    m = math.prod(x.shape[:-1])
+    out_shape = (*x.shape[:-1], n)
+
+    def out(t, name):
+        if t is None:
+            return torch.empty(out_shape, dtype=torch.bfloat16, device=x.device)
+        _on(t, x, name)
+        if t.dtype != torch.bfloat16 or t.numel() != m * n:
+            raise ValueError(f"{name} must be a bfloat16 tensor of m * n elements")
+        return t
+
+    h, s, u = out(h, "h"), out(s, "s"), out(u, "u")
+    if g is not None or store_g:
+        g = out(g, "g")
+    z, rstd = _norm_outs(x, m, k, z, rstd)
+    codes = _codes_out(m * n, x.device, codes)
+    with _device_of(x):   # launches go to the tensors' GPU
+        _check("msrms_linear_swiglu_fwd", lib().msrms_linear_swiglu_fwd(
+            BF16, m, n, k, float(eps), _ptr(x), _ptr(w_gate), _ptr(w_up), _ptr(h), _ptr(s), _ptr(u),
+            _ptr(codes), _ptr(g) if g is not None else None, _ptr(z), _ptr(rstd), _stream(x, stream)))
+    return (h, s, u, codes, z, rstd, g) if g is not None else (h, s, u, codes, z, rstd)

@@ -78,6 +78,7 @@ struct Tile {
   static constexpr int kOperandElems = kStages * kStageElems;
   static constexpr int kLdsElems =
       (kOperandElems > BM * kEpiRow) ? kOperandElems : BM * kEpiRow;
+  static constexpr int kLdsElemsNorm = kLdsElems + 2 * BM;   // + the rows' rstd (fp32)
   static constexpr int kLA = BM / kRowsPerLoad / kWaves, kLB = BN / kRowsPerLoad / kWaves;
   static constexpr int kLoadsPerStage = kLA + kLB;
   static constexpr int kEpiThreadsPerRow = BN / 16;
@@ -86,7 +87,7 @@ struct Tile {
   static_assert((BM / kRowsPerLoad) % kWaves == 0 && (BN / kRowsPerLoad) % kWaves == 0,
                 "load blocks per wave");
   static_assert(kThreads % kEpiThreadsPerRow == 0, "epilogue mapping");
-  static_assert(kLdsElems * 2 <= 160 * 1024, "LDS per block");
+  static_assert(kLdsElemsNorm * 2 <= 160 * 1024, "LDS per block");
   static_assert(kStages >= 2 && (kStages - 1) * kLoadsPerStage <= 63, "vector-memory counter range");
 };
 
@@ -160,9 +161,13 @@ struct LinArgs {
   uint32_t* codes;
   uint16_t* z;
   int64_t M, N, K;
+  // Norm in front (NORM): x is the norm's input, rstd its per-row statistic (fp32), and
+  // zn [M x K] receives the norm's output z = bf16(x rstd).
+  const float* rstd;
+  uint16_t* zn;
 };
 
-template <class C, int ACT, bool GLU>
+template <class C, int ACT, bool GLU, bool NORM>
 __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) {
   using A = ActOf<ACT>;
   constexpr int BM = C::BM, BN = C::BN, TM = C::TM, TN = C::TN, kWaves = C::kWaves;
@@ -179,8 +184,16 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
   const int wm = wave / C::WN, wn = wave % C::WN;
 
   int64_t tm, tn;
-  block_tile((M + BM - 1) / BM, (N + kOut - 1) / kOut, tm, tn);
+  const int64_t tiles_n = (N + kOut - 1) / kOut;
+  block_tile((M + BM - 1) / BM, tiles_n, tm, tn);
   const int64_t m0 = tm * BM, n0 = tn * kOut;
+
+  // Norm in front: the block's rows' rstd in LDS past the operand / epilogue area
+  // (visible after the first barrier).
+  float* rs_lds = reinterpret_cast<float*>(lds + C::kLdsElems);
+  if constexpr (NORM) {
+    for (int r = tid; r < BM; r += C::kThreads) rs_lds[r] = (m0 + r < M) ? a.rstd[m0 + r] : 0.0f;
+  }
 
   f32x16 acc[TM][TN];
 #pragma unroll
@@ -259,6 +272,44 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
         acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[buf][i], fb[buf][j], acc[i][j], 0, 0, 0);
   };
 
+  // Norm in front: the norm's output z = bf16(x rstd), stored with the norm kernel's
+  // rounding (fp32 product, round to nearest even). The x columns of K step kt of this
+  // row tile are written by the block with tn = kt mod tiles_n, from x read again (it
+  // has just streamed through the caches), outside the K loop, whose body stays
+  // branch-free. The block's first chunk is requested before the last K step's matrix
+  // products, which hide the loads. Consecutive lanes take consecutive 16-byte chunks of
+  // a row; rows beyond M and columns beyond K read through an empty range (zeros).
+  constexpr int kZv = NORM ? BM * (C::BK / 8) / C::kThreads : 1;
+  u32x4 zv[kZv];
+  auto z_chunk_load = [&](int64_t kt) {
+    constexpr int U = C::BK / 8;
+    const auto r = make_rsrc(x + m0 * K, rows_x * K * 2);
+#pragma unroll
+    for (int i = 0; i < kZv; ++i) {
+      const int q = tid + i * C::kThreads;
+      const int64_t col = kt * C::BK + (q % U) * 8;
+      zv[i] = __builtin_amdgcn_raw_buffer_load_b128(
+          r, col < K ? uint32_t(((q / U) * K + col) * 2) : kOutOfRange, 0, 0);
+    }
+  };
+  auto z_chunk_store = [&](int64_t kt) {
+    constexpr int U = C::BK / 8;
+#pragma unroll
+    for (int i = 0; i < kZv; ++i) {
+      const int q = tid + i * C::kThreads;
+      const int rr = q / U;
+      const int64_t col = kt * C::BK + (q % U) * 8;
+      if (m0 + rr < M && col < K) {
+        const float rsr = rs_lds[rr];
+        float f[8];
+        BF16::unpack(zv[i], f);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) f[e] = f[e] * rsr;
+        *reinterpret_cast<u32x4*>(a.zn + (m0 + rr) * K + col) = BF16::pack(f);
+      }
+    }
+  };
+
   // Loads of steps at or beyond the last one read zeros into buffers that are no longer
   // needed, so every step sees the same number of loads in flight and the waits are
   // constants (the vector-memory counter counts only these loads in the loop).
@@ -294,6 +345,9 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
       }
     }
     const uint16_t* S = stage_ptr(kt_count - 1);
+    if constexpr (NORM) {
+      if (tn < kt_count) z_chunk_load(tn);
+    }
 #pragma unroll
     for (int kk = 0; kk < C::kSlices; ++kk) {
       if (kk + 1 < C::kSlices) read(S, kk + 1, (kk + 1) & 1);
@@ -302,6 +356,13 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
     }
   }
   __syncthreads();   // waits for every load (including the zero-filling ones) and read
+
+  if constexpr (NORM) {
+    for (int64_t kt = tn; kt < kt_count; kt += tiles_n) {
+      if (kt != tn) z_chunk_load(kt);
+      z_chunk_store(kt);
+    }
+  }
 
   // Epilogue, part 1: bias, rounding to bf16, the tile into LDS (row-major, padded).
   // Gated form: columns [0, BN/2) hold g, [BN/2, BN) hold u of the same output columns.
@@ -316,7 +377,9 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = wm * TM * 32 + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-        E[row * C::kEpiRow + col] = uint16_t(pack_bf16x2(acc[i][j][r] + bj, 0.0f) & 0xffffu);
+        // norm in front: z W^T = rstd (x W^T), the row scale applied to the fp32 sum
+        const float v = NORM ? __builtin_fmaf(acc[i][j][r], rs_lds[row], bj) : acc[i][j][r] + bj;
+        E[row * C::kEpiRow + col] = uint16_t(pack_bf16x2(v, 0.0f) & 0xffffu);
       }
   }
   __syncthreads();
@@ -369,12 +432,12 @@ __global__ __launch_bounds__(C::kThreads) void linear_act_fwd_kernel(LinArgs a) 
   }
 }
 
-template <class C, int ACT, bool GLU>
+template <class C, int ACT, bool GLU, bool NORM = false>
 hipError_t launch_tile(const LinArgs& a, hipStream_t s) {
   constexpr int kOut = GLU ? C::BN / 2 : C::BN;
   const int64_t blocks = ((a.M + C::BM - 1) / C::BM) * ((a.N + kOut - 1) / kOut);
   if (blocks > 0x7fffffff) return hipErrorInvalidValue;
-  const size_t lds = size_t(C::kLdsElems) * 2;
+  const size_t lds = size_t(NORM ? C::kLdsElemsNorm : C::kLdsElems) * 2;
   // More than 64 KiB of dynamic LDS must be allowed explicitly, per kernel and device;
   // the attribute is set on the first launch on each device.
   constexpr int kMaxDevices = 64;
@@ -384,12 +447,12 @@ hipError_t launch_tile(const LinArgs& a, hipStream_t s) {
   if (e != hipSuccess) return e;
   if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
   if (!attr_set[dev].load(std::memory_order_acquire)) {
-    e = hipFuncSetAttribute(reinterpret_cast<const void*>(linear_act_fwd_kernel<C, ACT, GLU>),
+    e = hipFuncSetAttribute(reinterpret_cast<const void*>(linear_act_fwd_kernel<C, ACT, GLU, NORM>),
                             hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
     if (e != hipSuccess) return e;
     attr_set[dev].store(true, std::memory_order_release);
   }
-  hipLaunchKernelGGL((linear_act_fwd_kernel<C, ACT, GLU>), dim3(unsigned(blocks)),
+  hipLaunchKernelGGL((linear_act_fwd_kernel<C, ACT, GLU, NORM>), dim3(unsigned(blocks)),
                      dim3(C::kThreads), lds, s, a);
   return hipGetLastError();
 }
@@ -421,7 +484,7 @@ hipError_t launch_linear_act_fwd(int act, int64_t M, int64_t N, int64_t K, const
                                  void* z, hipStream_t s) {
   lin::LinArgs a{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), nullptr,
                  static_cast<const uint16_t*>(bias), static_cast<uint16_t*>(y), nullptr,
-                 nullptr, codes, static_cast<uint16_t*>(z), M, N, K};
+                 nullptr, codes, static_cast<uint16_t*>(z), M, N, K, nullptr, nullptr};
   const bool big = use_big_tiles(M, N);
   using lin::BigTile;
   using lin::SmallTile;
@@ -437,11 +500,45 @@ hipError_t launch_linear_glu_fwd(int64_t M, int64_t N, int64_t K, const void* x,
   lin::LinArgs a{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_gate),
                  static_cast<const uint16_t*>(w_up), nullptr, static_cast<uint16_t*>(h),
                  static_cast<uint16_t*>(s_out), static_cast<uint16_t*>(u), codes,
-                 static_cast<uint16_t*>(g), M, N, K};
+                 static_cast<uint16_t*>(g), M, N, K, nullptr, nullptr};
   // Each block covers half as many output columns as its tile width.
   const bool big = use_big_tiles(M, 2 * N);
   return big ? lin::launch_tile<lin::BigTile, kSilu, true>(a, s)
              : lin::launch_tile<lin::SmallTile, kSilu, true>(a, s);
+}
+
+hipError_t launch_linear_rms_act_fwd(int act, int64_t M, int64_t N, int64_t K, float eps,
+                                     const void* x, const void* w, const void* bias, void* y,
+                                     uint32_t* codes, void* pre, void* z_norm, float* rstd,
+                                     hipStream_t s) {
+  hipError_t e = launch_norm_fwd(false, true, M, K, eps, x, nullptr, rstd, true, s);
+  if (e != hipSuccess) return e;
+  lin::LinArgs a{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w), nullptr,
+                 static_cast<const uint16_t*>(bias), static_cast<uint16_t*>(y), nullptr,
+                 nullptr, codes, static_cast<uint16_t*>(pre), M, N, K, rstd,
+                 static_cast<uint16_t*>(z_norm)};
+  const bool big = use_big_tiles(M, N);
+  using lin::BigTile;
+  using lin::SmallTile;
+  using lin::launch_tile;
+  if (act == kGelu)
+    return big ? launch_tile<BigTile, kGelu, false, true>(a, s) : launch_tile<SmallTile, kGelu, false, true>(a, s);
+  return big ? launch_tile<BigTile, kSilu, false, true>(a, s) : launch_tile<SmallTile, kSilu, false, true>(a, s);
+}
+
+hipError_t launch_linear_rms_glu_fwd(int64_t M, int64_t N, int64_t K, float eps, const void* x,
+                                     const void* w_gate, const void* w_up, void* h, void* s_out,
+                                     void* u, uint32_t* codes, void* g, void* z_norm, float* rstd,
+                                     hipStream_t s) {
+  hipError_t e = launch_norm_fwd(false, true, M, K, eps, x, nullptr, rstd, true, s);
+  if (e != hipSuccess) return e;
+  lin::LinArgs a{static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w_gate),
+                 static_cast<const uint16_t*>(w_up), nullptr, static_cast<uint16_t*>(h),
+                 static_cast<uint16_t*>(s_out), static_cast<uint16_t*>(u), codes,
+                 static_cast<uint16_t*>(g), M, N, K, rstd, static_cast<uint16_t*>(z_norm)};
+  const bool big = use_big_tiles(M, 2 * N);
+  return big ? lin::launch_tile<lin::BigTile, kSilu, true, true>(a, s)
+             : lin::launch_tile<lin::SmallTile, kSilu, true, true>(a, s);
 }
 
 }  // namespace lmbp

@@ -299,6 +299,80 @@ lmbp_status linear_swiglu_fwd_impl(lmbp_dtype dt, int64_t m, int64_t n, int64_t 
                                               static_cast<hipStream_t>(stream)));
 }
 
+// The norm-in-front forms: x [m x k] is MS-RMSNorm's input, z [m x k] and rstd [m] its
+// outputs; the rest as for the plain forms. k >= 8 (a norm needs a row).
+lmbp_status check_norm_in_front(int64_t m, int64_t n, int64_t k, float eps, const void* x,
+                                const void* z, const float* rstd) {
+  const int64_t lim = int64_t(1) << 31;
+  if (m < 0 || n < 0 || k < 0 || m >= lim || n >= lim || k >= lim) return LMBP_EINVAL;
+  if (n % 16 != 0 || k % 8 != 0 || k > (int64_t(1) << 21)) return LMBP_EINVAL;
+  if (!(std::isfinite(eps) && eps > 0.0f)) return LMBP_EINVAL;
+  if (m > 0 && k == 0) return LMBP_EINVAL;
+  if (m > 0 && (!x || !z || !rstd)) return LMBP_EINVAL;
+  if ((x && !aligned(x, 16)) || (z && !aligned(z, 16)) || (rstd && !aligned(rstd, 4))) return LMBP_EINVAL;
+  return LMBP_OK;
+}
+
+lmbp_status msrms_linear_act_fwd_impl(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
+                                      float eps, const void* x, const void* w, const void* bias,
+                                      void* y, uint32_t* codes, void* pre, void* z, float* rstd,
+                                      void* stream) {
+  if (!known_dtype(dt) || dt != LMBP_BF16) return LMBP_EDTYPE;
+  if (act != LMBP_ACT_GELU && act != LMBP_ACT_SILU) return LMBP_EINVAL;
+  const lmbp_status st = check_norm_in_front(m, n, k, eps, x, z, rstd);
+  if (st != LMBP_OK) return st;
+  if (m == 0 || n == 0) return LMBP_OK;
+  if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (!y || !codes || !w) return LMBP_EINVAL;
+  if (!aligned(w, 16) || !aligned(y, 16) || !aligned(codes, 4) || (bias && !aligned(bias, 2)) ||
+      (pre && !aligned(pre, 16)))
+    return LMBP_EINVAL;
+  const uint64_t mn = uint64_t(m) * uint64_t(n), mk = uint64_t(m) * uint64_t(k);
+  const Span outs[5] = {span(y, mn * 2), span(codes, lmbp_codes_bytes(int64_t(mn))), span(z, mk * 2),
+                        span(rstd, uint64_t(m) * 4), span(pre, pre ? mn * 2 : 0)};
+  const Span ins[3] = {span(x, mk * 2), span(w, uint64_t(n) * uint64_t(k) * 2),
+                       span(bias, bias ? uint64_t(n) * 2 : 0)};
+  for (int i = 0; i < 5; ++i) {
+    for (int j = i + 1; j < 5; ++j)
+      if (overlaps(outs[i], outs[j])) return LMBP_EOVERLAP;
+    for (const Span& in : ins)
+      if (overlaps(outs[i], in)) return LMBP_EOVERLAP;
+  }
+  return from_hip(lmbp::launch_linear_rms_act_fwd(act == LMBP_ACT_GELU ? lmbp::kGelu : lmbp::kSilu, m, n,
+                                                  k, eps, x, w, bias, y, codes, pre, z, rstd,
+                                                  static_cast<hipStream_t>(stream)));
+}
+
+lmbp_status msrms_linear_swiglu_fwd_impl(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, float eps,
+                                         const void* x, const void* w_gate, const void* w_up, void* h,
+                                         void* s, void* u, uint32_t* codes, void* g, void* z,
+                                         float* rstd, void* stream) {
+  if (!known_dtype(dt) || dt != LMBP_BF16) return LMBP_EDTYPE;
+  const lmbp_status st = check_norm_in_front(m, n, k, eps, x, z, rstd);
+  if (st != LMBP_OK) return st;
+  if (m == 0 || n == 0) return LMBP_OK;
+  if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
+  if (!h || !s || !u || !codes || !w_gate || !w_up) return LMBP_EINVAL;
+  const void* sixteen[] = {w_gate, w_up, h, s, u};
+  for (const void* p : sixteen)
+    if (!aligned(p, 16)) return LMBP_EINVAL;
+  if (!aligned(codes, 4) || (g && !aligned(g, 16))) return LMBP_EINVAL;
+  const uint64_t mn = uint64_t(m) * uint64_t(n), mk = uint64_t(m) * uint64_t(k);
+  const Span outs[7] = {span(h, mn * 2), span(s, mn * 2), span(u, mn * 2),
+                        span(codes, lmbp_codes_bytes(int64_t(mn))), span(z, mk * 2),
+                        span(rstd, uint64_t(m) * 4), span(g, g ? mn * 2 : 0)};
+  const Span ins[3] = {span(x, mk * 2), span(w_gate, uint64_t(n) * uint64_t(k) * 2),
+                       span(w_up, uint64_t(n) * uint64_t(k) * 2)};
+  for (int i = 0; i < 7; ++i) {
+    for (int j = i + 1; j < 7; ++j)
+      if (overlaps(outs[i], outs[j])) return LMBP_EOVERLAP;
+    for (const Span& in : ins)
+      if (overlaps(outs[i], in)) return LMBP_EOVERLAP;
+  }
+  return from_hip(lmbp::launch_linear_rms_glu_fwd(m, n, k, eps, x, w_gate, w_up, h, s, u, codes, g, z,
+                                                  rstd, static_cast<hipStream_t>(stream)));
+}
+
 }  // namespace
 
 extern "C" {
@@ -383,6 +457,19 @@ lmbp_status linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, co
                               const void* w_gate, const void* w_up, void* h, void* s, void* u,
                               uint32_t* codes, void* g, void* stream) {
   return linear_swiglu_fwd_impl(dt, m, n, k, x, w_gate, w_up, h, s, u, codes, g, stream);
+}
+
+lmbp_status msrms_linear_act_fwd(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k, float eps,
+                                 const void* x, const void* w, const void* bias, void* y, uint32_t* codes,
+                                 void* pre, void* z, float* rstd, void* stream) {
+  return msrms_linear_act_fwd_impl(act, dt, m, n, k, eps, x, w, bias, y, codes, pre, z, rstd, stream);
+}
+
+lmbp_status msrms_linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, float eps,
+                                    const void* x, const void* w_gate, const void* w_up, void* h, void* s,
+                                    void* u, uint32_t* codes, void* g, void* z, float* rstd, void* stream) {
+  return msrms_linear_swiglu_fwd_impl(dt, m, n, k, eps, x, w_gate, w_up, h, s, u, codes, g, z, rstd,
+                                      stream);
 }
 
 lmbp_status lmbp_copy(const void* src, void* dst, int64_t bytes, void* stream) {

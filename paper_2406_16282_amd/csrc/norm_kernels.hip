@@ -133,16 +133,18 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_fwd_vec(const void* x,
   const float rs = rsqrtf(q[0] / float(cols) + eps);
   if (!active) return;
 
+  if (z != nullptr) {   // null z: statistics only (the pre-pass of the fused norm-linear)
 #pragma unroll
-  for (int j = 0; j < VPL; ++j) {
-    opaque(v[j]);
-    const int idx = j * TPR + t;
-    if (idx < nv) {
-      float f[E];
-      IO::unpack(v[j], f);
+    for (int j = 0; j < VPL; ++j) {
+      opaque(v[j]);
+      const int idx = j * TPR + t;
+      if (idx < nv) {
+        float f[E];
+        IO::unpack(v[j], f);
 #pragma unroll
-      for (int e = 0; e < E; ++e) f[e] = (LN ? (f[e] - pivot) - mean_d : f[e]) * rs;
-      stb16<LMBP_NORM_STORE_CPOL>(vec_rsrc(z, vbase, nv), idx, IO::pack(f));
+        for (int e = 0; e < E; ++e) f[e] = (LN ? (f[e] - pivot) - mean_d : f[e]) * rs;
+        stb16<LMBP_NORM_STORE_CPOL>(vec_rsrc(z, vbase, nv), idx, IO::pack(f));
+      }
     }
   }
   if (t == 0) rstd[row] = rs;
@@ -295,7 +297,8 @@ __global__ __launch_bounds__(norm_block<WPR>()) void norm_fwd_pipe(const void* x
     }
     row_sums<WPR>(q, &red[par][1]);
     const float rs = rsqrtf(q[0] / float(cols) + eps);
-    const auto rz = row_rsrc(z, active ? row * nv * 16 : 0, active ? nv * 16 : 0);
+    // a null z (statistics only) gets an empty resource: its stores are dropped
+    const auto rz = row_rsrc(z, active ? row * nv * 16 : 0, (active && z != nullptr) ? nv * 16 : 0);
 #pragma unroll
     for (int j = 0; j < VPL; ++j) {
       opaque(v[j]);
@@ -340,9 +343,11 @@ __global__ __launch_bounds__(256) void norm_fwd_any(const void* x, void* z, floa
   }
   const float var = block_sum(s2, red) / float(cols);
   const float rs = rsqrtf(var + eps);
-  for (int64_t k = tid; k < cols; k += blockDim.x) {
-    const float f = IO::load1(x, base + k);
-    IO::store1(z, base + k, (LN ? (f - pivot) - mean_d : f) * rs);
+  if (z != nullptr) {
+    for (int64_t k = tid; k < cols; k += blockDim.x) {
+      const float f = IO::load1(x, base + k);
+      IO::store1(z, base + k, (LN ? (f - pivot) - mean_d : f) * rs);
+    }
   }
   if (tid == 0) rstd[row] = rs;
 }

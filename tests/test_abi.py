@@ -166,6 +166,45 @@ def test_linear_swiglu_errors(L):
     assert f(B.BF16, 4, 32, 16, x, wg, wu, h, s, u, c, c - 16, None) == B.EOVERLAP  # g on codes
 
 
+def test_msrms_linear_act_errors(L):
+    f = L.msrms_linear_act_fwd
+    G = B.ACT_SILU
+    # m = 4, n = 32, k = 16: x / z 128 B, w 1024 B, bias 64 B, y 256 B, codes 32 B, rstd 16 B
+    x, w, bias, y, c, z, r, a = (P + 4096 * i for i in range(8))
+    assert f(G, B.FP32, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z, r, None) == B.EDTYPE
+    assert f(9, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z, r, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 32, 16, 0.0, x, w, bias, y, c, None, z, r, None) == B.EINVAL            # eps
+    assert f(G, B.BF16, 4, 32, 16, float("nan"), x, w, bias, y, c, None, z, r, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 24, 16, 1e-5, x, w, bias, y, c, None, z, r, None) == B.EINVAL           # n % 16
+    assert f(G, B.BF16, 4, 32, 12, 1e-5, x, w, bias, y, c, None, z, r, None) == B.EINVAL           # k % 8
+    assert f(G, B.BF16, 4, 32, 0, 1e-5, x, w, bias, y, c, None, z, r, None) == B.EINVAL            # no row
+    assert f(G, B.BF16, 0, 32, 16, 1e-5, x, w, bias, y, c, None, z, r, None) == B.OK               # empty
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, None, r, None) == B.EINVAL        # z required
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z, None, None) == B.EINVAL        # rstd required
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z + 8, r, None) == B.EINVAL       # alignment
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z, r + 2, None) == B.EINVAL
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, x, r, None) == B.EOVERLAP         # z on x
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z, y + 64, None) == B.EOVERLAP    # rstd on y
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, None, z, w, None) == B.EOVERLAP         # rstd on w
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, a + 2, z, r, None) == B.EINVAL          # pre alignment
+    assert f(G, B.BF16, 4, 32, 16, 1e-5, x, w, bias, y, c, y + 64, z, r, None) == B.EOVERLAP       # pre on y
+
+
+def test_msrms_linear_swiglu_errors(L):
+    f = L.msrms_linear_swiglu_fwd
+    x, wg, wu, h, s, u, c, z, r = (P + 4096 * i for i in range(9))
+    g = None
+    assert f(B.FP32, 4, 32, 16, 1e-5, x, wg, wu, h, s, u, c, g, z, r, None) == B.EDTYPE
+    assert f(B.BF16, 4, 32, 16, -1.0, x, wg, wu, h, s, u, c, g, z, r, None) == B.EINVAL
+    assert f(B.BF16, 4, 32, 12, 1e-5, x, wg, wu, h, s, u, c, g, z, r, None) == B.EINVAL
+    assert f(B.BF16, 0, 32, 16, 1e-5, x, wg, wu, h, s, u, c, g, z, r, None) == B.OK
+    assert f(B.BF16, 4, 32, 16, 1e-5, x, wg, wu, h, s, u, c, g, None, r, None) == B.EINVAL
+    assert f(B.BF16, 4, 32, 16, 1e-5, x, wg, wu, h, s, u, c, g, h, r, None) == B.EOVERLAP      # z on h
+    assert f(B.BF16, 4, 32, 16, 1e-5, x, wg, wu, h, s, u, c, g, z, c, None) == B.EOVERLAP      # rstd on codes
+    assert f(B.BF16, 4, 32, 16, 1e-5, x, wg, wu, h, s, u, c, u + 16, z, r, None) == B.EOVERLAP  # g on u
+    assert f(B.BF16, 4, 32, 16, 1e-5, x, wg, wu, h, s, u, c, P + 4096 * 9 + 2, z, r, None) == B.EINVAL
+
+
 def test_copy_errors(L):
     assert L.lmbp_copy(P, P + 4096, -1, None) == B.EINVAL
     assert L.lmbp_copy(P, P + 4096, 0, None) == B.OK

@@ -155,6 +155,27 @@ def test_linear_guards():
         for (buf, _), what in zip(bufs, ("h", "s", "u", "g")):
             check_guards(buf, m * n, 0, f"swiglu linear {what} {m}x{n}x{k}")
         check_guards(cb, words, 0, f"swiglu linear codes {m}x{n}x{k}")
+        # MS-RMSNorm in front: z [m, k] and rstd [m] as well
+        zb, z = guarded(m * k, torch.bfloat16)
+        rb, r = guarded(m, torch.float32)
+        yb, y = guarded(m * n, torch.bfloat16)
+        pb, pre = guarded(m * n, torch.bfloat16)
+        cb, c = guarded(words, torch.int32)
+        lmbp.msrms_linear_act_fwd(x, w, 1e-5, bias=b, act="silu", y=y, codes=c, z=z.view(m, k), rstd=r, pre=pre)
+        for buf, cnt, what in ((yb, m * n, "y"), (pb, m * n, "pre"), (cb, words, "codes"), (zb, m * k, "z"),
+                               (rb, m, "rstd")):
+            check_guards(buf, cnt, 0, f"norm linear {what} {m}x{n}x{k}")
+        bufs = [guarded(m * n, torch.bfloat16) for _ in range(4)]
+        zb, z = guarded(m * k, torch.bfloat16)
+        rb, r = guarded(m, torch.float32)
+        cb, c = guarded(words, torch.int32)
+        lmbp.msrms_linear_swiglu_fwd(x, w, wu, 1e-5, h=bufs[0][1], s=bufs[1][1], u=bufs[2][1], codes=c,
+                                     g=bufs[3][1], z=z.view(m, k), rstd=r)
+        for (buf, _), what in zip(bufs, ("h", "s", "u", "g")):
+            check_guards(buf, m * n, 0, f"norm swiglu linear {what} {m}x{n}x{k}")
+        check_guards(cb, words, 0, f"norm swiglu linear codes {m}x{n}x{k}")
+        check_guards(zb, m * k, 0, f"norm swiglu linear z {m}x{n}x{k}")
+        check_guards(rb, m, 0, f"norm swiglu linear rstd {m}x{n}x{k}")
 
 
 def test_copy_guards():

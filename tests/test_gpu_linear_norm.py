@@ -1,0 +1,167 @@
+"""GPU parity of MS-RMSNorm fused into the linear layer (msrms_linear_act_fwd,
+msrms_linear_swiglu_fwd) against the CPU oracle, through the C ABI.
+
+The norm's outputs z and rstd must be the bytes the stand-alone norm kernel writes.
+The pre-activation is bf16(rstd (x W^T) + b): the row scale applied to the fp32 sums of
+the products of x (the layer sees the normalised row before its storage rounding), so it
+is compared with the oracle's z W^T + b, z as computed, under a bound derived from the
+arithmetic (below); codes must lie in the range admissible under that bound and nearly
+always equal the oracle's; y and codes must be exactly what the activation kernels make of
+the stored pre-activation.
+
+Bound: with X = sum_t x_t w_t (products of bf16 values, exact in fp32) and
+S = sum_t |x_t w_t|, the fp32 sum is within (k + 1) 2^-24 S of X in any order; the GPU's
+rstd differs from the oracle's by |rs - r|, the fused multiply-add adds one fp32 rounding,
+and the bf16 rounding at most 2^-8 of the magnitude:
+    acc = (k + 1) 2^-24 (rs S + |b|) + |X| |rs - r| + 2^-24 |p|,
+    bound = acc + 2^-8 (|p| + acc)."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2406_16282_amd as lmbp
+from paper_2406_16282_amd import inputs
+from compare import assert_codes_equal, assert_mixed, assert_rel
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+EPS = float(np.float32(1e-5))
+THRESH = {"gelu": oracle.GELU_C, "silu": oracle.SILU_C}
+
+
+def T(a):
+    return inputs.storage_to_torch(a, DEV)
+
+
+def H(t):
+    return inputs.torch_to_storage(t)
+
+
+def norm_equal_to_kernel(x, z, rstd, label):
+    z_k, r_k = lmbp.msrms_fwd(T(x), EPS)
+    torch.cuda.synchronize()
+    assert np.array_equal(H(z_k), z), f"{label}: z differs from msrms_fwd's bytes"
+    assert np.array_equal(H(r_k), rstd), f"{label}: rstd differs from msrms_fwd's bits"
+
+
+def pre_bound(x, w, b, rows, rs_gpu, p, r_o):
+    k = x.shape[1]
+    xd = oracle.decode(x[rows], "bf16")
+    wd = oracle.decode(w, "bf16")
+    S = oracle.linear(np.abs(xd), np.abs(wd))
+    X = oracle.linear(xd, wd)
+    bb = np.zeros(w.shape[0]) if b is None else np.abs(oracle.decode(b, "bf16"))
+    rs = rs_gpu[rows].astype(np.float64)[:, None]
+    acc = (k + 1) * 2.0 ** -24 * (rs * S + bb[None, :]) + np.abs(X) * np.abs(rs - r_o[:, None]) \
+        + 2.0 ** -24 * np.abs(p)
+    return acc + 2.0 ** -8 * (np.abs(p) + acc)
+
+
+def check_pre(got_bits, p, p_s, bound, label):
+    got = oracle.decode(got_bits, "bf16")
+    err = np.abs(got - p)
+    assert np.all(err <= bound), f"{label}: pre-activation outside the bound (worst err/bound " \
+                                 f"{np.max(err / bound):.3g})"
+    assert np.mean(got_bits == p_s) >= 0.99, f"{label}: correctly rounded for too few elements"
+
+
+def check_codes(codes_rows, p, bound, c_o, act, label):
+    lo = oracle.segment_code(p - bound, THRESH[act])
+    hi = oracle.segment_code(p + bound, THRESH[act])
+    assert np.all((lo <= codes_rows) & (codes_rows <= hi)), f"{label}: a code outside the admissible range"
+    ref = oracle.unpack_codes(c_o, p.size).reshape(p.shape)
+    assert np.mean(codes_rows == ref) >= 0.999, f"{label}: codes equal the oracle's for too few elements"
+
+
+def run_act(m, n, k, act, bias, label, rows=None, scale=1.0):
+    print(f"[linear-norm] act {label}: m={m} n={n} k={k} act={act} bias={bias}", flush=True)
+    x = inputs.normal((m, k), scale, "bf16", tensor_id=inputs.NORM_X, block=m + n + k)
+    w = inputs.normal((n, k), 2.0 * k ** -0.5, "bf16", tensor_id=inputs.LIN_W, block=m + n + k)
+    b = inputs.normal((n,), 0.1, "bf16", tensor_id=inputs.LIN_B, block=m + n + k) if bias else None
+    y, codes, z, rstd, pre = (H(t) for t in lmbp.msrms_linear_act_fwd(
+        T(x), T(w), EPS, bias=None if b is None else T(b), act=act, store_pre=True))
+    torch.cuda.synchronize()
+    norm_equal_to_kernel(x, z, rstd, label)
+    # y and codes: the activation kernel's on the stored pre-activation
+    fwd = lmbp.regelu2_fwd if act == "gelu" else lmbp.resilu2_fwd
+    y2, c2 = fwd(T(pre))
+    torch.cuda.synchronize()
+    assert np.array_equal(H(y2), y) and np.array_equal(H(c2), codes), f"{label}: y / codes not the activation's"
+    rows = np.arange(m) if rows is None else rows
+    p, p_s, y_o, c_o, z_s, r_o = oracle.msrms_linear_act_fwd(x[rows], w, b, act, EPS)
+    assert_rel(rstd[rows].astype(np.float64), r_o, 1e-5, f"{label} rstd", floor=0.0)
+    assert_mixed(oracle.decode(z[rows], "bf16"), oracle.decode(z_s, "bf16"), 1e-2, f"{label} z")
+    bound = pre_bound(x, w, b, rows, rstd, p, r_o)
+    check_pre(pre.reshape(m, n)[rows], p, p_s, bound, label)
+    check_codes(oracle.unpack_codes(codes, m * n).reshape(m, n)[rows], p, bound, c_o, act, label)
+    assert_mixed(oracle.decode(y.reshape(m, n)[rows], "bf16"), y_o, 1e-2, f"{label} y")
+
+
+SHAPES = [
+    (128, 128, 64),      # one tile, one K step
+    (200, 272, 200),     # ragged m, n and K (several K steps, z shared out over tile columns)
+    (300, 96, 1024),     # 16 K steps over 1 tile column: every step written by the same block
+    (1, 16, 8),          # one row, the shortest K
+    (130, 2048, 520),    # many tile columns, K steps fewer than the columns
+]
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+@pytest.mark.parametrize("m,n,k", SHAPES)
+def test_act(m, n, k, act):
+    run_act(m, n, k, act, bias=True, label=f"{m}x{n}x{k}")
+
+
+def test_act_no_bias_large_tiles():
+    """Large enough for the 256 x 256 tiles, ragged in every dimension; sampled rows
+    (including the ragged last row tile)."""
+    m, n, k = 8000, 8208, 520
+    rows = np.unique(np.concatenate([[0, 255, 256, 7935, 7936, 7999], np.random.default_rng(4).integers(0, m, 20)]))
+    run_act(m, n, k, "silu", bias=False, label="large tiles", rows=rows)
+
+
+def run_glu(m, n, k, label, rows=None, outliers=False):
+    print(f"[linear-norm] swiglu {label}: m={m} n={n} k={k}", flush=True)
+    if outliers:
+        x = inputs.outlier_mixture((m, k), "bf16", tensor_id=inputs.NORM_X)
+    else:
+        x = inputs.normal((m, k), 1.0, "bf16", tensor_id=inputs.NORM_X, block=m + n + k)
+    wg = inputs.normal((n, k), 2.0 * k ** -0.5, "bf16", tensor_id=inputs.LIN_W, block=m + n + k)
+    wu = inputs.normal((n, k), k ** -0.5, "bf16", tensor_id=inputs.LIN_B, block=m + n + k)
+    h, s, u, codes, z, rstd, g = (H(t) for t in lmbp.msrms_linear_swiglu_fwd(T(x), T(wg), T(wu), EPS,
+                                                                            store_g=True))
+    torch.cuda.synchronize()
+    norm_equal_to_kernel(x, z, rstd, label)
+    h2, s2, c2 = lmbp.reswiglu2_fwd(T(g), T(u))
+    torch.cuda.synchronize()
+    assert np.array_equal(H(h2), h) and np.array_equal(H(s2), s) and np.array_equal(H(c2), codes), \
+        f"{label}: h / s / codes not the SwiGLU kernel's on the stored g and u"
+    rows = np.arange(m) if rows is None else rows
+    gx, g_s, ux, u_s, h_o, s_o, c_o, z_s, r_o = oracle.msrms_linear_swiglu_fwd(x[rows], wg, wu, EPS)
+    assert_rel(rstd[rows].astype(np.float64), r_o, 1e-5, f"{label} rstd", floor=0.0)
+    bg = pre_bound(x, wg, None, rows, rstd, gx, r_o)
+    bu = pre_bound(x, wu, None, rows, rstd, ux, r_o)
+    check_pre(g.reshape(m, n)[rows], gx, g_s, bg, f"{label} g")
+    check_pre(u.reshape(m, n)[rows], ux, u_s, bu, f"{label} u")
+    check_codes(oracle.unpack_codes(codes, m * n).reshape(m, n)[rows], gx, bg, c_o, "silu", label)
+    assert_mixed(oracle.decode(h.reshape(m, n)[rows], "bf16"), h_o, 1e-2, f"{label} h")
+
+
+@pytest.mark.parametrize("m,n,k", [(128, 64, 64), (200, 208, 200), (257, 1024, 136)])
+def test_swiglu(m, n, k):
+    run_glu(m, n, k, f"{m}x{n}x{k}")
+
+
+def test_swiglu_llama7b_full_size_sampled():
+    """The LLaMA-7B MLP input side at full size: x [8192, 4096] through MS-RMSNorm into the
+    gate and up projections (11008); z and rstd compared in full with the norm kernel, the
+    rest on sampled rows."""
+    rows = np.unique(np.concatenate([[0, 8191], np.random.default_rng(9).integers(0, 8192, 14)]))
+    run_glu(8192, 11008, 4096, "llama7b", rows=rows)
+
+
+def test_swiglu_outlier_rows():
+    """Rows dominated by 1% outliers N(0, 30^2) (the LLaMA-13B workload's mixture)."""
+    run_glu(512, 512, 1024, "outliers", outliers=True)

@@ -79,3 +79,71 @@ def test_linear_swiglu_composition():
     assert np.array_equal(g_s, x) and np.array_equal(u_s, x)
     h_ref, s_ref, c_ref = oracle.reswiglu2_fwd(oracle.decode(x, "bf16"), oracle.decode(x, "bf16"))
     assert np.array_equal(h, h_ref) and np.array_equal(s, s_ref) and np.array_equal(codes, c_ref)
+
+
+# ------------------------------------------------ MS-RMSNorm in front of the layer
+
+def _torch_rms_then_linear(x, alpha, w, b, eps):
+    """RMSNorm with affine alpha, then Linear(w, b), in float64 torch."""
+    import torch
+    import torch.nn.functional as F
+    xt = torch.from_numpy(x)
+    z = F.rms_norm(xt, (x.shape[1],), weight=torch.from_numpy(alpha), eps=eps)
+    return F.linear(z, torch.from_numpy(w), None if b is None else torch.from_numpy(b)).numpy()
+
+
+@pytest.mark.parametrize("act", ["gelu", "silu"])
+def test_msrms_linear_against_torch_with_merged_affine(act):
+    """RMSNorm(alpha) then Linear(W, b) (torch float64) equals the oracle's MS-RMSNorm in
+    front of the merged layer W~ = W diag(alpha) (Sec. 5.2 eq. norm_linear). alpha holds
+    powers of two so that W~ is exactly representable in bf16, as the stored weight is."""
+    g = np.random.default_rng(21)
+    m, k, n = 6, 64, 48
+    eps = 1e-5
+    x = inputs.normal((m, k), 1.5, "bf16", tensor_id=inputs.NORM_X)
+    w = inputs.normal((n, k), 0.2, "bf16", tensor_id=inputs.LIN_W)
+    b = inputs.normal((n,), 0.1, "bf16", tensor_id=inputs.LIN_B)
+    alpha = 2.0 ** g.integers(-2, 3, k).astype(np.float64)
+    wd = oracle.decode(w, "bf16")
+    w_merged = inputs.to_storage(wd * alpha[None, :], "bf16")
+    assert np.array_equal(oracle.decode(w_merged, "bf16"), wd * alpha[None, :])
+    p, p_s, y, codes, z_s, rstd = oracle.msrms_linear_act_fwd(x, w_merged, b, act, eps)
+    ref = _torch_rms_then_linear(oracle.decode(x, "bf16"), alpha, wd, oracle.decode(b, "bf16"), eps)
+    np.testing.assert_allclose(p, ref, rtol=1e-12, atol=1e-12)
+    # the stored z and rstd are the stand-alone norm's; y and codes the activation's of p_s
+    z_o, r_o = oracle.msrms_fwd(oracle.decode(x, "bf16"), eps)
+    assert np.array_equal(z_s, oracle.encode(z_o, "bf16")) and np.array_equal(rstd, r_o)
+    fwd = oracle.regelu2_fwd if act == "gelu" else oracle.resilu2_fwd
+    y_ref, c_ref = fwd(oracle.decode(p_s, "bf16"))
+    assert np.array_equal(y, y_ref) and np.array_equal(codes, c_ref)
+
+
+def test_msrms_linear_swiglu_against_torch():
+    g = np.random.default_rng(22)
+    m, k, n = 5, 40, 32
+    eps = 1e-5
+    x = inputs.normal((m, k), 1.0, "bf16", tensor_id=inputs.NORM_X)
+    wg = inputs.normal((n, k), 0.3, "bf16", tensor_id=inputs.LIN_W)
+    wu = inputs.normal((n, k), 0.3, "bf16", tensor_id=inputs.LIN_B)
+    ones = np.ones(k)
+    gx, g_s, ux, u_s, h, s, codes, z_s, rstd = oracle.msrms_linear_swiglu_fwd(x, wg, wu, eps)
+    xd = oracle.decode(x, "bf16")
+    np.testing.assert_allclose(gx, _torch_rms_then_linear(xd, ones, oracle.decode(wg, "bf16"), None, eps),
+                               rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(ux, _torch_rms_then_linear(xd, ones, oracle.decode(wu, "bf16"), None, eps),
+                               rtol=1e-12, atol=1e-12)
+    h_ref, s_ref, c_ref = oracle.reswiglu2_fwd(oracle.decode(g_s, "bf16"), oracle.decode(u_s, "bf16"))
+    assert np.array_equal(h, h_ref) and np.array_equal(s, s_ref) and np.array_equal(codes, c_ref)
+
+
+def test_msrms_linear_uses_the_unrounded_norm_output():
+    """The pre-activation is taken from z as computed, not from its bf16 storage: with a
+    row whose z is not representable in bf16, the two differ and the oracle follows the
+    former."""
+    x = inputs.to_storage(np.array([[3.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0, 1.0]]), "bf16")
+    w = inputs.to_storage(np.eye(8)[:1].repeat(16, axis=0), "bf16")   # picks z[0], 16 outputs
+    eps = float(np.float32(1e-5))
+    p, p_s, _, _, z_s, rstd = oracle.msrms_linear_act_fwd(x, w, None, "silu", eps)
+    z_exact = 3.0 / np.sqrt((9.0 + 7.0) / 8.0 + eps)
+    assert np.allclose(p, z_exact, rtol=1e-14, atol=0)
+    assert oracle.decode(z_s, "bf16")[0, 0] != z_exact
