@@ -822,13 +822,37 @@ def main():
     torch.cuda.synchronize()
     copy_ms = a.elapsed_time(b) / args.steps
     del pairs
+
+    # The same plain copy at each kernel's own size (half its bytes read, half written),
+    # cold in the same way (three buffer pairs in rotation): what pure streaming of that
+    # many bytes costs per launch on this GPU, fixed per-launch cost included.
+    print("[bench] same-size copies", file=sys.stderr, flush=True)
+    copy_same_ms = {}
+    for n in names:
+        half = (nb[n] // 2) // 16 * 16
+        pairs = [(torch.ones(half, dtype=torch.uint8, device=dev),
+                  torch.empty(half, dtype=torch.uint8, device=dev)) for _ in range(3)]
+        for j in range(6):
+            src, dst = pairs[j % 3]
+            lmbp.copy_bytes(src, dst, stream=stream)
+        a, b = mk(), mk()
+        a.record(stream)
+        for j in range(args.steps):
+            src, dst = pairs[j % 3]
+            lmbp.copy_bytes(src, dst, stream=stream)
+        b.record(stream)
+        torch.cuda.synchronize()
+        copy_same_ms[n] = a.elapsed_time(b) / args.steps
+        del pairs
     gc.enable()
 
     bytes_step = sum(nb.values())
     value = bytes_step / (ms_step * 1e-3) / 1e9
     per_kernel = {n: {"us": round(per_kernel_ms[n] * 1e3, 2),
                       "bytes": nb[n],
-                      "GBps": round(nb[n] / (per_kernel_ms[n] * 1e-3) / 1e9, 1)}
+                      "GBps": round(nb[n] / (per_kernel_ms[n] * 1e-3) / 1e9, 1),
+                      "copy_same_bytes_us": round(copy_same_ms[n] * 1e3, 2),
+                      "copy_over_kernel": round(copy_same_ms[n] / per_kernel_ms[n], 3)}
                   for n in names}
     dominant = max(names, key=lambda n: per_kernel_ms[n])
     achieved = nb[dominant] / (per_kernel_ms[dominant] * 1e-3) / 1e9

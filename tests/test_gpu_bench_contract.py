@@ -40,6 +40,9 @@ def test_bench_prints_one_contract_line(flags):
     assert rf["frac"] == pytest.approx(rf["achieved"] / rf["peak"], abs=1e-4)
     assert 0.3 < rf["frac"] < 1.0
     assert rf["kernel"] in d["per_kernel"]
+    for rec in d["per_kernel"].values():   # the same-size plain copy is a streaming ceiling
+        assert rec["copy_same_bytes_us"] > 0
+        assert rec["copy_over_kernel"] == pytest.approx(rec["copy_same_bytes_us"] / rec["us"], abs=2e-3)
     # the metric's other ops, MS-LN and ReGELU2, on the ViT-B batch-64 bf16 shapes
     vit = d["pairs_vit_b_bs64_bf16"]
     assert set(vit) == {"msln", "regelu2"}
