@@ -250,6 +250,8 @@ lmbp_status linear_swiglu_fwd(lmbp_dtype dt, int64_t m, int64_t n, int64_t k, co
  *          linear_act_fwd's z).
  *   z    : m x k bf16, 16-byte aligned (required: the saved tensor).
  *   rstd : m fp32, 4-byte aligned.
+ * n == 0 (no output features) still writes z and rstd, by the stand-alone norm kernel;
+ * w, bias, y, codes and pre are then not used. m == 0 is a successful no-op.
  * No output may overlap another output or an input. The backward pass is the linear
  * layer's (or SwiGLU's) backward on the kept tensors, then msrms_bwd(dz, z, rstd).
  * ------------------------------------------------------------------------ */

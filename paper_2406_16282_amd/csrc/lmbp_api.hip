@@ -310,7 +310,19 @@ lmbp_status check_norm_in_front(int64_t m, int64_t n, int64_t k, float eps, cons
   if (m > 0 && k == 0) return LMBP_EINVAL;
   if (m > 0 && (!x || !z || !rstd)) return LMBP_EINVAL;
   if ((x && !aligned(x, 16)) || (z && !aligned(z, 16)) || (rstd && !aligned(rstd, 4))) return LMBP_EINVAL;
+  if (m == 0) return LMBP_OK;
+  const uint64_t mk = uint64_t(m) * uint64_t(k);
+  const Span sx = span(x, mk * 2), sz = span(z, mk * 2), sr = span(rstd, uint64_t(m) * 4);
+  if (overlaps(sx, sz) || overlaps(sx, sr) || overlaps(sz, sr)) return LMBP_EOVERLAP;
   return LMBP_OK;
+}
+
+// A layer with no output features (n == 0) still normalises its input: z and rstd come
+// from the stand-alone norm kernel (the same bytes the fused path writes).
+hipError_t norm_in_front_only(int64_t m, int64_t k, float eps, const void* x, void* z, float* rstd,
+                              void* stream) {
+  return lmbp::launch_norm_fwd(false, true, m, k, eps, x, z, rstd, true,
+                               static_cast<hipStream_t>(stream));
 }
 
 lmbp_status msrms_linear_act_fwd_impl(lmbp_act act, lmbp_dtype dt, int64_t m, int64_t n, int64_t k,
@@ -321,7 +333,8 @@ lmbp_status msrms_linear_act_fwd_impl(lmbp_act act, lmbp_dtype dt, int64_t m, in
   if (act != LMBP_ACT_GELU && act != LMBP_ACT_SILU) return LMBP_EINVAL;
   const lmbp_status st = check_norm_in_front(m, n, k, eps, x, z, rstd);
   if (st != LMBP_OK) return st;
-  if (m == 0 || n == 0) return LMBP_OK;
+  if (m == 0) return LMBP_OK;
+  if (n == 0) return from_hip(norm_in_front_only(m, k, eps, x, z, rstd, stream));
   if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
   if (!y || !codes || !w) return LMBP_EINVAL;
   if (!aligned(w, 16) || !aligned(y, 16) || !aligned(codes, 4) || (bias && !aligned(bias, 2)) ||
@@ -350,7 +363,8 @@ lmbp_status msrms_linear_swiglu_fwd_impl(lmbp_dtype dt, int64_t m, int64_t n, in
   if (!known_dtype(dt) || dt != LMBP_BF16) return LMBP_EDTYPE;
   const lmbp_status st = check_norm_in_front(m, n, k, eps, x, z, rstd);
   if (st != LMBP_OK) return st;
-  if (m == 0 || n == 0) return LMBP_OK;
+  if (m == 0) return LMBP_OK;
+  if (n == 0) return from_hip(norm_in_front_only(m, k, eps, x, z, rstd, stream));
   if (uint64_t(m) * uint64_t(n) > (uint64_t(1) << 60)) return LMBP_EINVAL;
   if (!h || !s || !u || !codes || !w_gate || !w_up) return LMBP_EINVAL;
   const void* sixteen[] = {w_gate, w_up, h, s, u};

@@ -165,3 +165,18 @@ def test_swiglu_llama7b_full_size_sampled():
 def test_swiglu_outlier_rows():
     """Rows dominated by 1% outliers N(0, 30^2) (the LLaMA-13B workload's mixture)."""
     run_glu(512, 512, 1024, "outliers", outliers=True)
+
+
+def test_no_output_features_still_normalises():
+    """n = 0: the layer has no outputs, but the call still writes the norm's z and rstd
+    (the stand-alone norm kernel's bytes), for both forms."""
+    m, k = 96, 264
+    print(f"[linear-norm] n = 0: m={m} k={k}", flush=True)
+    x = inputs.normal((m, k), 1.0, "bf16", tensor_id=inputs.NORM_X, block=m + k)
+    w = torch.empty((0, k), dtype=torch.bfloat16, device=DEV)
+    y, codes, z, rstd = lmbp.msrms_linear_act_fwd(T(x), w, EPS, act="silu")
+    h, s, u, codes2, z2, rstd2 = lmbp.msrms_linear_swiglu_fwd(T(x), w, w, EPS)
+    torch.cuda.synchronize()
+    assert y.numel() == 0 and codes.numel() == 0 and h.numel() == 0 and codes2.numel() == 0
+    norm_equal_to_kernel(x, H(z), H(rstd), "n = 0 act")
+    norm_equal_to_kernel(x, H(z2), H(rstd2), "n = 0 swiglu")
