@@ -18,7 +18,7 @@ import torch
 import oracle
 import paper_2406_16282_amd as lmbp
 from paper_2406_16282_amd import inputs
-from compare import assert_codes_equal, assert_mixed, assert_rel, bf16_ulp_distance
+from compare import NORMAL_MIN, assert_codes_equal, assert_mixed, assert_rel, bf16_ulp_distance
 
 pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
@@ -50,7 +50,7 @@ def check_exact(m, n, k, act, bias, label):
     assert_codes_equal(codes, c_o, f"{label} codes")
     y64 = oracle.decode(y, "bf16")
     assert_rel(y64, y_o, 1e-2, f"{label} y (strict)")
-    m_ = np.abs(y_o) >= 2.0 ** -60
+    m_ = np.abs(y_o) >= NORMAL_MIN
     d = bf16_ulp_distance(y, y_o)[m_]
     assert d.max() <= 1, f"{label}: y more than one bf16 step from the oracle"
     if d.size >= 1000:
