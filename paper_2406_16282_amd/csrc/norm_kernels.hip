@@ -383,7 +383,10 @@ __global__ __launch_bounds__(256) void norm_bwd_any(const void* dz, const void* 
 #define LMBP_NORM_TARGET_VPL 2  // preferred upper bound on vectors per thread
 #endif
 #ifndef LMBP_NORM_FWD_VPL
-#define LMBP_NORM_FWD_VPL LMBP_NORM_TARGET_VPL  // the forward kernel's target
+// The forward's target: 3 lets a 768-wide fp32 row (192 vectors) run on one wave with
+// three vectors per thread, and with it the persistent form (9% faster than two waves of
+// two vectors, a quarter of them idle); the backward was 3% slower that way.
+#define LMBP_NORM_FWD_VPL 3
 #endif
 #ifndef LMBP_NORM_BWD_VPL
 #define LMBP_NORM_BWD_VPL LMBP_NORM_TARGET_VPL  // the backward kernel's target

@@ -75,18 +75,22 @@ def test_parity(op, dtype, rows, cols, xs, gs, eps):
 
 
 # One width per launch shape of the register-tile path: (waves per row, vectors per
-# thread) = (1,1), (1,2), (2,2), (4,2), (4,3), (4,4), (4,6), (4,8), (4,12), (4,16).
-SHAPE_WIDTHS = {"bf16": [512, 1024, 2048, 4096, 5120, 8192, 12288, 16384, 24576, 32768],
-                "fp32": [256, 512, 1024, 2048, 2560, 4096, 6144, 8192, 12288, 16384]}
+# thread) = (1,1), (1,2), (2,2), (4,2), (4,3), (4,4), (4,6), (4,8), (4,12), (4,16), and
+# the forward's (1,3) and (2,3) (its target is 3 vectors per thread, the backward's 2:
+# those two widths run (2,2) and (4,2) backward).
+SHAPE_WIDTHS = {"bf16": [512, 1024, 2048, 4096, 5120, 8192, 12288, 16384, 24576, 32768, 1536, 3072],
+                "fp32": [256, 512, 1024, 2048, 2560, 4096, 6144, 8192, 12288, 16384, 768, 1536]}
 
 
+@pytest.mark.parametrize("cols", [512, 768])
 @pytest.mark.parametrize("dtype", ["bf16", "fp32"])
 @pytest.mark.parametrize("op", ["msln", "msrms"])
-def test_forward_row_groups_walked_by_persistent_blocks(op, dtype):
-    """Rows of one wave (here 512 wide) take the persistent forward: with many more row
-    groups than resident blocks, each block walks several groups with the next one's loads
-    in flight and alternating LDS slots; the row count leaves the last group partial."""
-    rows, cols = 24003, 512
+def test_forward_row_groups_walked_by_persistent_blocks(op, dtype, cols):
+    """Rows of one wave (512 or 768 wide: one to three vectors per thread) take the
+    persistent forward: with many more row groups than resident blocks, each block walks
+    several groups with the next one's loads in flight and alternating LDS slots; the row
+    count leaves the last group partial."""
+    rows = 24003
     x = inputs.normal((rows, cols), 1.0, dtype, tensor_id=inputs.NORM_X, block=11)
     dz = inputs.normal((rows, cols), 1.0, dtype, tensor_id=inputs.NORM_DZ, block=11)
     check_norm(op, dtype, x, dz, 1e-5, f"persistent({rows}x{cols})")
