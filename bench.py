@@ -714,6 +714,13 @@ def main():
             return [lambda: nfwd(self.x, eps, z=self.z, rstd=self.rstd, stream=stream), act[0], act[1],
                     lambda: nbwd(self.dz, self.z, self.rstd, dx=self.dx, stream=stream)]
 
+    # Python's garbage collector runs once here, before the tensor sets are built (GPU
+    # copies), and is then off through the timed loops: a collection takes tens of ms, during
+    # which the GPU would sit idle right before (or, inside the loops, within) the timed
+    # region; the sets' copies and the priming launches run right before the warm-up.
+    gc.collect()
+    gc.disable()
+
     # Three tensor sets. Step k runs the forward kernels on set k % 3 and the backward
     # kernels on set (k - 1) % 3, i.e. the backward consumes saved state written one
     # full step (about 1.1 GB of traffic) earlier, as in training where a layer's
@@ -746,11 +753,6 @@ def main():
         torch.cuda.synchronize()
         return graph
 
-    # Python's garbage collector runs once here and is then off from the warm-up through
-    # the timed loops: a collection takes tens of ms, during which the GPU would sit idle
-    # right before (or, inside the loops, within) the timed region.
-    gc.collect()
-    gc.disable()
     k0 = args.warmup
     graph = None if not args.graph else captured(lambda: [step(k0 + k, kc) for k in range(args.steps)])
     for st in ks:          # every set holds valid saved state before the first step

@@ -50,11 +50,14 @@ def check_exact(m, n, k, act, bias, label):
     assert_codes_equal(codes, c_o, f"{label} codes")
     y64 = oracle.decode(y, "bf16")
     assert_rel(y64, y_o, 1e-2, f"{label} y (strict)")
+    # every normal output within one bf16 step; >= 99% correctly rounded away from the
+    # far-negative tail (GELU z < -8, SiLU z < -85), where only the one-step rule applies
     m_ = np.abs(y_o) >= NORMAL_MIN
-    d = bf16_ulp_distance(y, y_o)[m_]
-    assert d.max() <= 1, f"{label}: y more than one bf16 step from the oracle"
-    if d.size >= 1000:
-        assert np.mean(d == 0) >= 0.99, f"{label}: y correctly rounded for too few elements"
+    d = bf16_ulp_distance(y, y_o)
+    assert d[m_].max() <= 1, f"{label}: y more than one bf16 step from the oracle"
+    bulk = m_ & (oracle.decode(z_s, "bf16").reshape(d.shape) >= (-8.0 if act == "gelu" else -85.0))
+    if bulk.sum() >= 1000:
+        assert np.mean(d[bulk] == 0) >= 0.99, f"{label}: y correctly rounded for too few elements"
 
 
 EXACT_SHAPES = [
