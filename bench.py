@@ -826,26 +826,30 @@ def main():
     del pairs
 
     # The same plain copy at each kernel's own size (half its bytes read, half written),
-    # cold in the same way (three buffer pairs in rotation): what pure streaming of that
-    # many bytes costs per launch on this GPU, fixed per-launch cost included.
+    # cold in the same way (three buffer pairs in rotation) and launched the same way as the
+    # per-kernel loop (replayed from a graph with --graph): what pure streaming of that many
+    # bytes costs per launch on this GPU, fixed per-launch cost included.
     print("[bench] same-size copies", file=sys.stderr, flush=True)
     copy_same_ms = {}
     for n in names:
         half = (nb[n] // 2) // 16 * 16
         pairs = [(torch.ones(half, dtype=torch.uint8, device=dev),
                   torch.empty(half, dtype=torch.uint8, device=dev)) for _ in range(3)]
+        copy = lambda j, st: lmbp.copy_bytes(pairs[j % 3][0], pairs[j % 3][1], stream=st)
         for j in range(6):
-            src, dst = pairs[j % 3]
-            lmbp.copy_bytes(src, dst, stream=stream)
+            copy(j, stream)
+        g_c = None if not args.graph else captured(lambda: [copy(j, None) for j in range(args.steps)])
         a, b = mk(), mk()
         a.record(stream)
-        for j in range(args.steps):
-            src, dst = pairs[j % 3]
-            lmbp.copy_bytes(src, dst, stream=stream)
+        if g_c is None:
+            for j in range(args.steps):
+                copy(j, stream)
+        else:
+            g_c.replay()
         b.record(stream)
         torch.cuda.synchronize()
         copy_same_ms[n] = a.elapsed_time(b) / args.steps
-        del pairs
+        del g_c, pairs
     gc.enable()
 
     bytes_step = sum(nb.values())
